@@ -1,0 +1,112 @@
+"""Workload configurations: shapes, dtypes, generator recipe and cost tables.
+
+The five graded workloads (``c0`` .. ``c4``) and two ungraded stress workloads
+(``s1``, ``s2``).  Costs are in arbitrary units; the drafting cost is 1.0
+everywhere.  The verification cost is given as a table ``C_v(0..cap)``, the
+form in which the method consumes it (a profiled, convex, non-decreasing
+function of the node count; the paper's cost model, Sec. 4.2 and Sec. 4.6).
+"""
+
+from __future__ import annotations
+
+import dataclasses
+from typing import Callable, Dict
+
+import numpy as np
+
+SEED_BASE = 260601813
+
+
+@dataclasses.dataclass(frozen=True)
+class Config:
+    name: str
+    B: int            # rounds per batch
+    L: int            # block positions per round
+    V: int            # vocabulary size
+    dtype: str        # "f32" or "bf16"
+    K: int            # top-K per position
+    cap: int          # budget cap (maximum number of draft nodes)
+    t_draft: float    # C_d
+    cost: str         # name of the C_v recipe, see ``cost_table``
+    mask: str         # "u8" (dense bytes) or "bits" (packed u32, LSB first)
+    recipe: str       # "normal", "peak" or "peak_temp"
+    seed: int
+
+    @property
+    def elem_bytes(self) -> int:
+        return 4 if self.dtype == "f32" else 2
+
+    @property
+    def row_bytes(self) -> int:
+        return self.V * self.elem_bytes
+
+    @property
+    def batch_bytes(self) -> int:
+        return self.B * self.L * self.V * self.elem_bytes
+
+    def replace(self, **kw) -> "Config":
+        return dataclasses.replace(self, **kw)
+
+
+def _quad(a: float, b: float) -> Callable[[np.ndarray], np.ndarray]:
+    return lambda n: 1.0 + a * n + b * n * n
+
+
+def _piecewise_c3(n: np.ndarray) -> np.ndarray:
+    # flat at 1.0 up to n = 64, slope 0.004 up to n = 256, slope 0.012 beyond
+    return np.where(n <= 64, 1.0,
+                    np.where(n <= 256, 1.0 + 0.004 * (n - 64),
+                             1.768 + 0.012 * (n - 256)))
+
+
+_COSTS: Dict[str, Callable[[np.ndarray], np.ndarray]] = {
+    "c0": _quad(0.01, 0.0005),
+    "c1": _quad(0.002, 0.00002),
+    "c3": _piecewise_c3,
+    "c4": _quad(0.001, 0.000005),
+    "const": lambda n: np.ones_like(n, dtype=np.float64),
+}
+
+
+def cost_table(cfg_or_name, cap: int | None = None) -> np.ndarray:
+    """C_v(0..cap) as float64, length cap + 1."""
+    if isinstance(cfg_or_name, Config):
+        name, cap = cfg_or_name.cost, cfg_or_name.cap if cap is None else cap
+    else:
+        name = cfg_or_name
+    n = np.arange(cap + 1, dtype=np.float64)
+    return np.ascontiguousarray(_COSTS[name](n), dtype=np.float64)
+
+
+V_FULL = 151936
+
+CONFIGS: Dict[str, Config] = {
+    "c0": Config("c0", B=1, L=4, V=1024, dtype="f32", K=4, cap=32, t_draft=1.0,
+                 cost="c0", mask="u8", recipe="normal", seed=SEED_BASE + 0),
+    "c1": Config("c1", B=64, L=16, V=V_FULL, dtype="bf16", K=8, cap=512, t_draft=1.0,
+                 cost="c1", mask="u8", recipe="peak", seed=SEED_BASE + 1),
+    "c2": Config("c2", B=1024, L=16, V=V_FULL, dtype="bf16", K=8, cap=512, t_draft=1.0,
+                 cost="c1", mask="u8", recipe="peak", seed=SEED_BASE + 2),
+    "c3": Config("c3", B=256, L=16, V=V_FULL, dtype="bf16", K=16, cap=1024, t_draft=1.0,
+                 cost="c3", mask="bits", recipe="peak_temp", seed=SEED_BASE + 3),
+    "c4": Config("c4", B=256, L=32, V=V_FULL, dtype="f32", K=16, cap=4096, t_draft=1.0,
+                 cost="c4", mask="bits", recipe="peak", seed=SEED_BASE + 4),
+}
+
+# Ungraded stress workloads: constant cost (always grows to the cap) and a
+# low-temperature regime that gives deep trees of a few hundred nodes.
+STRESS: Dict[str, Config] = {
+    "s1": Config("s1", B=256, L=32, V=V_FULL, dtype="f32", K=16, cap=4096, t_draft=1.0,
+                 cost="const", mask="bits", recipe="peak", seed=SEED_BASE + 11),
+    "s2": Config("s2", B=256, L=32, V=V_FULL, dtype="f32", K=16, cap=4096, t_draft=1.0,
+                 cost="c4", mask="bits", recipe="peak_cold", seed=SEED_BASE + 12),
+}
+
+
+def get_config(name: str) -> Config:
+    name = name.lower()
+    if name in CONFIGS:
+        return CONFIGS[name]
+    if name in STRESS:
+        return STRESS[name]
+    raise KeyError(f"unknown workload {name!r}; known: {sorted(CONFIGS) + sorted(STRESS)}")

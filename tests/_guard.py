@@ -1,0 +1,51 @@
+"""Input guard: redraw rounds whose tree decisions sit within a hair of a tie.
+
+A GPU log-normaliser differs from the oracle's fp64 value by rounding, which
+shifts every log prefix probability at depth d by the same tiny amount.  Such a
+shift can only change the output through a stop decision or a kept-versus-
+frontier comparison across depths whose margin is below it.  The guard keeps
+every such margin of a round at or above ``TAU`` (relative; 1e-6 is the gap the
+workloads require), redrawing the round with the next attempt of its seed
+until it passes.  Same-depth comparisons are exact on both sides and need no
+guard.
+"""
+
+from __future__ import annotations
+
+from typing import Dict, Tuple
+
+import numpy as np
+
+import oracle
+import synth
+
+TAU = 1e-6
+MAX_ATTEMPTS = 20
+
+
+def oracle_round(cfg: synth.Config, x: np.ndarray, pos_offset: int = 0, mask=None):
+    return oracle.build_round(x, cfg.dtype, cfg.K, cfg.t_draft, synth.cost_table(cfg), cfg.cap,
+                              pos_offset=pos_offset, mask=mask or cfg.mask)
+
+
+def guarded_round(cfg: synth.Config, b: int, tau: float = TAU, pos_offset: int = 0):
+    """(attempt, logits, oracle result) for round b, redrawn until its margins clear tau."""
+    for a in range(MAX_ATTEMPTS):
+        x = synth.draw_round(cfg, b, a)
+        r = oracle_round(cfg, x, pos_offset)
+        stop, gap = oracle.decision_margins(r.exp)
+        if stop >= tau and gap >= tau:
+            return a, x, r
+    raise RuntimeError(f"round {b} of {cfg.name} failed the guard {MAX_ATTEMPTS} times")
+
+
+def guarded_batch(cfg: synth.Config, rounds, tau: float = TAU, pos_offset: int = 0):
+    """Returns (attempts {b: a}, logits [n, L, V], [oracle results]) for the given rounds."""
+    attempts: Dict[int, int] = {}
+    xs, rs = [], []
+    for b in rounds:
+        a, x, r = guarded_round(cfg, b, tau, pos_offset)
+        attempts[b] = a
+        xs.append(x)
+        rs.append(r)
+    return attempts, np.stack(xs), rs
