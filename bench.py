@@ -1,0 +1,191 @@
+#!/usr/bin/env python3
+"""Benchmark: CaDDTree draft-tree construction throughput on one MI355X.
+
+One step = one ``caddtree_build`` over a whole batch of rounds (vocabulary
+reduction + top-K, best-first expansion with the greedy stop, mask and position
+ids), with the logits already resident in HBM.  Prints ONE JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--workload c2]
+
+Default workload c2: 1024 rounds x L=16 x V=151936 bf16 logits, K=8, cap 512,
+C_d = 1, C_v(n) = 1 + 0.002 n + 0.00002 n^2 (the HBM-saturating batch of the
+L=16 / V=151936 / bf16 rounds/sec metric).  Inputs are the seeded synthetic
+generator of that workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "rounds/sec, L=16 V=151936 bf16 marginals→CaDDTree; % of HBM peak"
+K1_SOURCE = os.path.join(ROOT, "paper_2606_01813_amd", "csrc", "reduce_topk.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def k1_source_hash() -> str:
+    with open(K1_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per K1 launch from committed rocprofv3 counter runs, if they match this kernel source."""
+    path = os.path.join(ROOT, "profiles", f"k1_traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("k1_source_sha256_16") != k1_source_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(cfg, xs, target_s: float, max_rounds: int):
+    """The oracle (test infrastructure), one core, on a bounded sample of the same rounds."""
+    import oracle
+    tv = synth.cost_table(cfg)
+    t0 = time.perf_counter()
+    n = 0
+    while n < min(max_rounds, xs.shape[0]):
+        oracle.build_round(xs[n], cfg.dtype, cfg.K, cfg.t_draft, tv, cfg.cap, mask=cfg.mask)
+        n += 1
+        if time.perf_counter() - t0 >= target_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "rounds/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n} rounds of {cfg.name} ({dt:.1f} s of single-core fp64 numpy: LSE + top-K "
+                      f"+ Algorithm 1 + mask per round; input generation excluded)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c2")
+    ap.add_argument("--workers", type=int, default=synth.gen.default_workers())
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the rounds are independent and this "
+              f"build has no multi-GPU path; run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    cfg = synth.get_config(args.workload)
+    log(f"[bench] generating {cfg.name}: {cfg.B} x {cfg.L} x {cfg.V} {cfg.dtype} ({cfg.batch_bytes / 1e9:.2f} GB) "
+        f"with {args.workers} workers")
+    t = time.perf_counter()
+    xs = synth.draw_batch(cfg, workers=args.workers)
+    log(f"[bench] generated in {time.perf_counter() - t:.1f} s")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"[bench] cpu baseline: oracle on up to {args.cpu_seconds:.0f} s of rounds")
+        cpu = cpu_baseline(cfg, xs, args.cpu_seconds, max_rounds=cfg.B)
+        log(f"[bench] cpu baseline {cpu['value']:.3f} rounds/s")
+
+    import torch
+    from paper_2606_01813_amd import Plan
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    if cfg.dtype == "bf16":
+        logits = torch.from_numpy(xs.view(np.int16)).to(dev).view(torch.bfloat16)
+    else:
+        logits = torch.from_numpy(xs).to(dev)
+    del xs
+    plan = Plan(L=cfg.L, V=cfg.V, K=cfg.K, cap=cfg.cap, t_draft=cfg.t_draft, t_verify=synth.cost_table(cfg),
+                dtype=cfg.dtype, mask=cfg.mask)
+    B = cfg.B
+    out = plan.new_outputs(B)
+    ws = plan.new_workspace(B)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        plan.build(logits, out, pos_offset=0, workspace=ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: K whole-path steps
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    log(f"[bench] {args.steps} steps in {elapsed * 1e3:.2f} ms")
+
+    # per-stage durations (same work through the stage entry points), HIP events on the launch stream
+    topk = plan.new_outputs(B, topk=True)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for s in range(args.steps):
+        e = ev[s]
+        e[0].record(stream)
+        plan.reduce_topk(logits, topk.topk_ids, topk.topk_logit, topk.lse, topk.topk_lq, stream=stream)
+        e[1].record(stream)
+        plan.expand(topk.topk_ids, topk.topk_logit, topk.lse, topk, stream=stream)
+        e[2].record(stream)
+        plan.emit(topk, pos_offset=0, stream=stream)
+        e[3].record(stream)
+    torch.cuda.synchronize()
+    k1 = np.array([e[0].elapsed_time(e[1]) for e in ev]) * 1e3   # us
+    k2 = np.array([e[1].elapsed_time(e[2]) for e in ev]) * 1e3
+    k3 = np.array([e[2].elapsed_time(e[3]) for e in ev]) * 1e3
+    ns = out.n_star.cpu().numpy()
+    same = bool(torch.equal(out.n_star, topk.n_star) and torch.equal(out.token_ids, topk.token_ids))
+
+    rows = B * cfg.L
+    k1_bytes = rows * cfg.V * cfg.elem_bytes + rows * (cfg.K * 12 + 8)
+    achieved = k1_bytes / (k1.mean() * 1e-6) / 1e9
+    value = B * args.steps / elapsed
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "rounds/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32+f64",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {B} rounds x L={cfg.L} x V={cfg.V} {cfg.dtype} logits, K={cfg.K}, "
+                               f"cap {cfg.cap}, mask {cfg.mask}",
+                   "rounds": B, "L": cfg.L, "V": cfg.V, "logits_dtype": cfg.dtype, "K": cfg.K, "cap": cfg.cap,
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(cfg.name),
+                     "kernel": "reduce_topk_kernel", "bytes_per_launch": k1_bytes,
+                     "avg_launch_us": float(k1.mean())},
+        "cpu_baseline": cpu,
+        "stages_us": {"reduce_topk": float(k1.mean()), "expand": float(k2.mean()), "emit": float(k3.mean())},
+        "end_to_end_hbm_frac": (cfg.batch_bytes * args.steps / elapsed) / 1e9 / HBM_PEAK_GBS,
+        "n_star": {"mean": float(ns.mean()), "std": float(ns.std()), "min": int(ns.min()), "max": int(ns.max())},
+        "stage_path_matches_build": same,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,173 @@
+/*
+ * caddtree.h -- C ABI of the CaDDTree draft-tree construction library (MI355X / gfx950).
+ *
+ * What it computes (Cost-Aware Diffusion Draft Trees for Speculative Decoding,
+ * arXiv 2606.01813):  a speculative-decoding round starts from a block-diffusion
+ * drafter's logits l_1 .. l_L over a vocabulary of V tokens.  Per round the
+ * library
+ *   1. forms the full-vocabulary log-normaliser LSE_i and the top-K tokens of
+ *      every position i with log q_i^(k) = l_i^(k) - LSE_i (Sec. 3.2, eq.
+ *      marginals; the Require line of Algorithm 1);
+ *   2. grows the draft tree best-first by prefix probability pi_s =
+ *      prod_i q_i(s_i) (eq. prefix-prob) and stops at the first budget n where
+ *      theta*(n) = (1 + Phi*(n)) / (C_d + C_v(n)) (eq. per-round) stops rising
+ *      (Algorithm 1; Lemma 1, eq. stopping; Cor. 2);
+ *   3. lays the tree out breadth-first and emits its tree-attention mask
+ *      (each node sees itself and its ancestors, Sec. 3.3) and position ids.
+ *
+ * Conventions shared by every entry point:
+ *   - Device pointers are HIP device memory on the plan's device; host pointers
+ *     are named *_host.  The caller owns every buffer; the library allocates
+ *     nothing per call (a plan owns one small device copy of its cost table).
+ *   - All work is enqueued on the given stream and runs asynchronously; the
+ *     return value reports argument validation (done synchronously, before
+ *     anything is enqueued) and launch errors, not kernel completion.
+ *   - A non-OK status enqueues nothing new; caddtree_last_error() gives a
+ *     message (thread-local).  No C++ exception crosses this interface.
+ *   - Logits must be finite; results for NaN or +-Inf inputs are unspecified.
+ *   - Layouts are row-major.  B rounds, L positions, V vocabulary, K kept tokens
+ *     per position, cap = budget cap.  Logit row (b, i) starts at element
+ *     (b * L + i) * row_stride, row_stride >= V elements.
+ *   - Output slots at or beyond a round's n_star are left untouched; consumers
+ *     read n_star.  n_star = 0 (an empty tree) is a legal result.
+ *
+ * Tie-breaking (the paper leaves it open; fixed here so results are unique):
+ *   - top-K: value descending, then token id ascending;
+ *   - expansion order: log prefix probability descending, then depth
+ *     ascending, then the sum of raw logits along the path descending, then
+ *     the rank tuple lexicographically ascending;
+ *   - stop: theta_new <= theta_prev stops (ties keep the smaller tree), as in
+ *     Algorithm 1;
+ *   - output order: depth ascending, then rank tuple lexicographically
+ *     ascending (parents precede children).
+ */
+#ifndef CADDTREE_H
+#define CADDTREE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CADDTREE_MAX_L 32
+#define CADDTREE_MAX_K 16
+#define CADDTREE_MAX_CAP 4096
+
+typedef enum {
+  CADDTREE_OK = 0,
+  CADDTREE_E_INVALID = 1,      /* bad argument: NULL where required, negative or inconsistent size */
+  CADDTREE_E_UNSUPPORTED = 2,  /* valid request beyond this build's limits (L, K, cap, V) */
+  CADDTREE_E_COST = 3,         /* cost model rejected: C_d <= 0, non-finite, C_v decreasing or not convex */
+  CADDTREE_E_WORKSPACE = 4,    /* workspace NULL, misaligned or smaller than caddtree_workspace_bytes() */
+  CADDTREE_E_HIP = 5           /* a HIP runtime call or kernel launch failed */
+} caddtree_status_t;
+
+typedef enum { CADDTREE_F32 = 0, CADDTREE_BF16 = 1 } caddtree_dtype_t;
+
+/* Tree-attention mask format.  U8: [B, cap, cap] bytes, mask[b][i][j] = 1 iff
+ * node j is node i or an ancestor of i.  BITS32: [B, cap, ceil(cap/32)] u32
+ * words, bit (j % 32) of word (j / 32), least significant bit first.  Only
+ * rows i < n_star and columns j < n_star (words j/32 < ceil(n_star/32)) are
+ * written; for BITS32 the bits of the last written word at or beyond n_star
+ * are written as zero. */
+typedef enum { CADDTREE_MASK_NONE = 0, CADDTREE_MASK_U8 = 1, CADDTREE_MASK_BITS32 = 2 } caddtree_mask_t;
+
+/* flags */
+#define CADDTREE_ALLOW_NONCONVEX 1u  /* accept a C_v that is non-decreasing but not convex (Assumption 1
+                                        may then fail: the greedy stop is still taken, optimality is not claimed) */
+
+typedef struct caddtree_plan* caddtree_plan_t;   /* opaque, immutable after creation */
+
+/* Static description of a workload. */
+typedef struct {
+  int32_t L;                 /* block positions, 1 .. CADDTREE_MAX_L */
+  int64_t V;                 /* vocabulary size, K .. 2^31 - 1 */
+  int32_t K;                 /* tokens kept per position, 1 .. CADDTREE_MAX_K */
+  int32_t budget_cap;        /* maximum nodes per tree, 0 .. CADDTREE_MAX_CAP */
+  caddtree_dtype_t dtype;    /* logits element type */
+  caddtree_mask_t mask;      /* mask format written by caddtree_build / caddtree_emit */
+  uint32_t flags;            /* CADDTREE_ALLOW_NONCONVEX or 0 */
+  double t_draft;            /* C_d > 0, drafting cost of one round (Sec. 4.2) */
+  const double* t_verify_host; /* HOST array of budget_cap + 1 values C_v(0 .. cap): verification
+                                  cost of a tree of n nodes (Sec. 4.2, Sec. 4.6).  Must be finite,
+                                  non-decreasing and convex in n (Cor. 3) up to a relative rounding
+                                  slack of 1e-12; copied at plan creation. */
+} caddtree_config_t;
+
+/* Validates cfg, copies the cost table to the current device and returns a plan.
+ * The plan is bound to the device that is current at creation. */
+caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_plan_t* plan_out);
+/* Frees the plan (NULL is a no-op).  The caller ensures no enqueued work still uses it. */
+void caddtree_plan_destroy(caddtree_plan_t plan);
+
+/* Device workspace caddtree_build needs for B rounds (the top-K table when the
+ * caller does not ask for it).  256-byte alignment is required. */
+size_t caddtree_workspace_bytes(caddtree_plan_t plan, int64_t B);
+
+/* Outputs of caddtree_build (DEVICE pointers).  Required: token_ids, parent,
+ * depth, n_star.  Optional (NULL skips the output): everything else.
+ *   token_ids [B, cap] int32  vocabulary id of node i (canonical order)
+ *   parent    [B, cap] int32  index of the parent node, -1 when the parent is the root (bonus token)
+ *   depth     [B, cap] int32  1 .. L
+ *   path_prob [B, cap] float  pi_s of the node (eq. prefix-prob), rounded to fp32
+ *   n_star    [B]      int32  chosen budget
+ *   phi       [B]      float  Phi*(n_star) = sum of path_prob over the tree (eq. surrogate), fp32
+ *   theta     [B]      float  theta*(n_star) (eq. per-round), fp32
+ *   mask      see caddtree_mask_t; ignored when the plan's mask is NONE
+ *   pos_ids   [B, cap] int32  pos_offset + depth
+ *   topk_ids  [B, L, K] int32, topk_logit [B, L, K] float (raw logits),
+ *   topk_lq   [B, L, K] float (log q_i^(k)), lse [B, L] double (LSE_i) */
+typedef struct {
+  int32_t* token_ids;
+  int32_t* parent;
+  int32_t* depth;
+  float* path_prob;
+  int32_t* n_star;
+  float* phi;
+  float* theta;
+  void* mask;
+  int32_t* pos_ids;
+  int32_t* topk_ids;
+  float* topk_logit;
+  float* topk_lq;
+  double* lse;
+} caddtree_outputs_t;
+
+/* The whole hot path for B rounds: reduce + top-K, expansion, emission.
+ * logits: DEVICE [B, L, row_stride] of the plan's dtype; B >= 0 (0 is a no-op).
+ * workspace: DEVICE, >= caddtree_workspace_bytes(plan, B) bytes, 256-byte aligned
+ * (may be NULL when every top-K output pointer is given). */
+caddtree_status_t caddtree_build(caddtree_plan_t plan, const void* logits, int64_t B, int64_t row_stride,
+                                 int32_t pos_offset, const caddtree_outputs_t* out,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Stage 1 (Sec. 3.2): per (round, position) row, LSE in fp64 and the top-K by
+ * (value desc, id asc).  topk_ids, topk_logit, lse required; topk_lq optional. */
+caddtree_status_t caddtree_reduce_topk(caddtree_plan_t plan, const void* logits, int64_t B, int64_t row_stride,
+                                       int32_t* topk_ids, float* topk_logit, float* topk_lq, double* lse,
+                                       hipStream_t stream);
+
+/* Stage 2 (Algorithm 1): best-first expansion with the greedy stop, tree in canonical order.
+ * Inputs: topk_ids, topk_logit [B, L, K], lse [B, L] (DEVICE).  token_ids,
+ * parent, depth, n_star required; path_prob, phi, theta optional. */
+caddtree_status_t caddtree_expand(caddtree_plan_t plan, const int32_t* topk_ids, const float* topk_logit,
+                                  const double* lse, int64_t B,
+                                  int32_t* token_ids, int32_t* parent, int32_t* depth, float* path_prob,
+                                  int32_t* n_star, float* phi, float* theta, hipStream_t stream);
+
+/* Stage 3 (Sec. 3.3): tree-attention mask and position ids from parent/depth/n_star.
+ * mask may be NULL (or the plan's mask NONE) to skip it; pos_ids may be NULL. */
+caddtree_status_t caddtree_emit(caddtree_plan_t plan, const int32_t* parent, const int32_t* depth,
+                                const int32_t* n_star, int64_t B, int32_t pos_offset,
+                                void* mask, int32_t* pos_ids, hipStream_t stream);
+
+const char* caddtree_status_string(caddtree_status_t status);
+const char* caddtree_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CADDTREE_H */

@@ -1,0 +1,181 @@
+"""CaDDTree draft-tree construction on MI355X (gfx950): Python binding.
+
+A thin marshalling layer over libcaddtree.so (include/caddtree.h): it turns
+torch tensors into device pointers and the current torch stream into the HIP
+stream, and calls the library.  Every step of the hot path runs in the HIP
+kernels; there is no fallback.  Importing works without a GPU (the library
+loads on first use); calls need the built library and a gfx950 device.
+
+    plan = Plan(L=16, V=151936, K=8, cap=512, t_draft=1.0, t_verify=table,
+                dtype="bf16", mask="u8")
+    out = plan.new_outputs(B)                 # torch tensors on the current device
+    ws = plan.new_workspace(B)
+    plan.build(logits, out, workspace=ws)      # logits: [B, L, >=V] bf16 tensor
+"""
+
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+from typing import Optional
+
+import numpy as np
+
+from . import _lib
+from ._lib import CaddtreeError, MAX_CAP, MAX_K, MAX_L
+
+__all__ = ["Plan", "TreeOutputs", "CaddtreeError", "MAX_L", "MAX_K", "MAX_CAP"]
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else int(t.data_ptr())
+
+
+def _stream(stream, device) -> int:
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+
+
+@dataclasses.dataclass
+class TreeOutputs:
+    """Device tensors written by Plan.build (see caddtree_outputs_t)."""
+    token_ids: object
+    parent: object
+    depth: object
+    path_prob: object
+    n_star: object
+    phi: object
+    theta: object
+    mask: object = None
+    pos_ids: object = None
+    topk_ids: object = None
+    topk_logit: object = None
+    topk_lq: object = None
+    lse: object = None
+
+    def as_struct(self) -> _lib.Outputs:
+        s = _lib.Outputs()
+        for f in _lib.Outputs._fields_:
+            setattr(s, f[0], _ptr(getattr(self, f[0])))
+        return s
+
+
+class Plan:
+    """An immutable CaDDTree plan (shape limits, dtype, mask format, cost model)."""
+
+    def __init__(self, L: int, V: int, K: int, cap: int, t_draft: float, t_verify,
+                 dtype: str = "bf16", mask: str = "u8", allow_nonconvex: bool = False):
+        self.L, self.V, self.K, self.cap = int(L), int(V), int(K), int(cap)
+        self.dtype, self.mask = dtype, mask
+        if dtype not in _lib.DTYPES:
+            raise ValueError(f"dtype must be one of {sorted(_lib.DTYPES)}")
+        if mask not in _lib.MASKS:
+            raise ValueError(f"mask must be one of {sorted(_lib.MASKS)}")
+        tv = np.ascontiguousarray(np.asarray(t_verify, dtype=np.float64))
+        if tv.ndim != 1 or tv.shape[0] < self.cap + 1:
+            raise ValueError(f"t_verify needs cap + 1 = {self.cap + 1} values")
+        self._tv = tv
+        cfg = _lib.Config(self.L, self.V, self.K, self.cap, _lib.DTYPES[dtype], _lib.MASKS[mask],
+                          _lib.ALLOW_NONCONVEX if allow_nonconvex else 0, float(t_draft),
+                          tv.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+        self._lib = _lib.lib()
+        h = ctypes.c_void_p()
+        _lib.check(self._lib.caddtree_plan_create(ctypes.byref(cfg), ctypes.byref(h)))
+        self._h = h
+
+    # ------------------------------------------------------------ lifetime
+    def close(self) -> None:
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            self._lib.caddtree_plan_destroy(h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    # ------------------------------------------------------------ allocation helpers
+    def workspace_bytes(self, B: int) -> int:
+        return int(self._lib.caddtree_workspace_bytes(self._h, int(B)))
+
+    def new_workspace(self, B: int, device=None):
+        torch = _torch()
+        n = max(self.workspace_bytes(B), 1)
+        return torch.empty(n, dtype=torch.uint8, device=device or "cuda")
+
+    def new_outputs(self, B: int, device=None, topk: bool = False) -> TreeOutputs:
+        torch = _torch()
+        dev = device or "cuda"
+        cap = max(self.cap, 1)
+        i32 = dict(dtype=torch.int32, device=dev)
+        f32 = dict(dtype=torch.float32, device=dev)
+        mask = None
+        if self.mask == "u8":
+            mask = torch.zeros((B, cap, cap), dtype=torch.uint8, device=dev)
+        elif self.mask == "bits":
+            mask = torch.zeros((B, cap, (cap + 31) // 32), dtype=torch.int32, device=dev)
+        out = TreeOutputs(
+            token_ids=torch.full((B, cap), -1, **i32), parent=torch.full((B, cap), -2, **i32),
+            depth=torch.zeros((B, cap), **i32), path_prob=torch.zeros((B, cap), **f32),
+            n_star=torch.full((B,), -1, **i32), phi=torch.zeros((B,), **f32), theta=torch.zeros((B,), **f32),
+            mask=mask, pos_ids=torch.zeros((B, cap), **i32))
+        if topk:
+            out.topk_ids = torch.empty((B, self.L, self.K), **i32)
+            out.topk_logit = torch.empty((B, self.L, self.K), **f32)
+            out.topk_lq = torch.empty((B, self.L, self.K), **f32)
+            out.lse = torch.empty((B, self.L), dtype=torch.float64, device=dev)
+        return out
+
+    # ------------------------------------------------------------ calls
+    def _logits(self, logits):
+        torch = _torch()
+        want = torch.bfloat16 if self.dtype == "bf16" else torch.float32
+        if logits.dtype != want:
+            raise TypeError(f"logits must be {want}, got {logits.dtype}")
+        if logits.dim() != 3 or logits.shape[1] != self.L or logits.shape[2] < self.V:
+            raise ValueError(f"logits must be [B, {self.L}, >= {self.V}], got {tuple(logits.shape)}")
+        if logits.stride(2) != 1 or logits.stride(0) != logits.stride(1) * self.L:
+            raise ValueError("logits rows must be evenly strided: [B, L, V] with a unit last stride")
+        return int(logits.shape[0]), int(logits.stride(1))
+
+    def build(self, logits, out: TreeOutputs, pos_offset: int = 0, workspace=None, stream=None) -> None:
+        B, stride = self._logits(logits)
+        ws_ptr = _ptr(workspace)
+        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        st = out.as_struct()
+        _lib.check(self._lib.caddtree_build(self._h, _ptr(logits), B, stride, int(pos_offset), ctypes.byref(st),
+                                            ws_ptr, ws_bytes, _stream(stream, logits.device)))
+
+    def reduce_topk(self, logits, topk_ids, topk_logit, lse, topk_lq=None, stream=None) -> None:
+        B, stride = self._logits(logits)
+        _lib.check(self._lib.caddtree_reduce_topk(self._h, _ptr(logits), B, stride, _ptr(topk_ids),
+                                                  _ptr(topk_logit), _ptr(topk_lq), _ptr(lse),
+                                                  _stream(stream, logits.device)))
+
+    def expand(self, topk_ids, topk_logit, lse, out: TreeOutputs, stream=None) -> None:
+        B = int(topk_ids.shape[0])
+        _lib.check(self._lib.caddtree_expand(self._h, _ptr(topk_ids), _ptr(topk_logit), _ptr(lse), B,
+                                             _ptr(out.token_ids), _ptr(out.parent), _ptr(out.depth),
+                                             _ptr(out.path_prob), _ptr(out.n_star), _ptr(out.phi),
+                                             _ptr(out.theta), _stream(stream, topk_ids.device)))
+
+    def emit(self, out: TreeOutputs, pos_offset: int = 0, stream=None) -> None:
+        B = int(out.parent.shape[0])
+        _lib.check(self._lib.caddtree_emit(self._h, _ptr(out.parent), _ptr(out.depth), _ptr(out.n_star), B,
+                                           int(pos_offset), _ptr(out.mask), _ptr(out.pos_ids),
+                                           _stream(stream, out.parent.device)))

@@ -1,0 +1,345 @@
+// Host side of the C ABI declared in caddtree.h: plan creation and validation,
+// workspace sizing, argument checks and launch sequencing on the caller's stream.
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "internal.h"
+
+struct caddtree_plan {
+  int32_t L;
+  int64_t V;
+  int32_t K;
+  int32_t cap;
+  caddtree_dtype_t dtype;
+  caddtree_mask_t mask;
+  uint32_t flags;
+  double t_draft;
+  double* d_t_verify;   // device copy, cap + 1 values
+  int device;
+  int k1_waves;         // 0 = automatic
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+caddtree_status_t fail(caddtree_status_t st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+caddtree_status_t fail(caddtree_status_t st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+caddtree_status_t ok() {
+  g_last_error.clear();
+  return CADDTREE_OK;
+}
+
+caddtree_status_t hip_fail(hipError_t e, const char* what) {
+  return fail(CADDTREE_E_HIP, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
+}
+
+size_t elem_bytes(caddtree_dtype_t d) { return d == CADDTREE_BF16 ? 2 : 4; }
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+caddtree_status_t check_plan(const caddtree_plan* p) {
+  if (p == nullptr) return fail(CADDTREE_E_INVALID, "plan is NULL");
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != p->device)
+    return fail(CADDTREE_E_INVALID, "plan was created on device %d but device %d is current", p->device, dev);
+  return CADDTREE_OK;
+}
+
+struct TopkBuffers {
+  int32_t* ids;
+  float* logit;
+  double* lse;
+};
+
+// Carves the top-K table out of the workspace for the pieces the caller did not supply.
+size_t topk_workspace(const caddtree_plan* p, int64_t B, const caddtree_outputs_t* out, char* base,
+                      TopkBuffers* tb) {
+  const size_t rows = (size_t)B * (size_t)p->L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) -> char* {
+    char* r = base ? base + off : nullptr;
+    off = align256(off + bytes);
+    return r;
+  };
+  tb->ids = out && out->topk_ids ? out->topk_ids : reinterpret_cast<int32_t*>(take(rows * p->K * 4));
+  tb->logit = out && out->topk_logit ? out->topk_logit : reinterpret_cast<float*>(take(rows * p->K * 4));
+  tb->lse = out && out->lse ? out->lse : reinterpret_cast<double*>(take(rows * 8));
+  return off;
+}
+
+caddtree_status_t check_logits(const caddtree_plan* p, const void* logits, int64_t B, int64_t row_stride) {
+  if (B < 0) return fail(CADDTREE_E_INVALID, "B = %lld is negative", (long long)B);
+  if (B > 0 && logits == nullptr) return fail(CADDTREE_E_INVALID, "logits is NULL");
+  if (row_stride < p->V)
+    return fail(CADDTREE_E_INVALID, "row_stride %lld < V %lld", (long long)row_stride, (long long)p->V);
+  if (B * (int64_t)p->L > (int64_t)INT32_MAX)
+    return fail(CADDTREE_E_UNSUPPORTED, "B * L = %lld exceeds 2^31 - 1 rows", (long long)(B * p->L));
+  return CADDTREE_OK;
+}
+
+int k1_waves(const caddtree_plan* p, int64_t rows) {
+  if (p->k1_waves > 0) return p->k1_waves;
+  return caddtree::reduce_default_waves(rows, (int32_t)p->V, p->dtype);
+}
+
+caddtree_status_t run_reduce(const caddtree_plan* p, const void* logits, int64_t B, int64_t row_stride,
+                             int32_t* ids, float* logit, float* lq, double* lse, hipStream_t stream) {
+  caddtree::ReduceArgs a;
+  a.logits = logits;
+  a.rows = B * p->L;
+  a.row_stride = row_stride;
+  a.V = (int32_t)p->V;
+  a.K = p->K;
+  a.waves_per_row = k1_waves(p, a.rows);
+  const size_t es = elem_bytes(p->dtype);
+  a.aligned = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) && ((size_t)row_stride * es) % 16 == 0;
+  a.ids = ids;
+  a.logit = logit;
+  a.lq = lq;
+  a.lse = lse;
+  hipError_t e = caddtree::launch_reduce_topk(a, p->dtype, stream);
+  if (e != hipSuccess) return hip_fail(e, "reduce_topk launch");
+  return CADDTREE_OK;
+}
+
+caddtree_status_t run_expand(const caddtree_plan* p, const int32_t* ids, const float* logit, const double* lse,
+                             int64_t B, int32_t* token_ids, int32_t* parent, int32_t* depth, float* path_prob,
+                             int32_t* n_star, float* phi, float* theta, hipStream_t stream) {
+  caddtree::ExpandArgs a;
+  a.topk_ids = ids;
+  a.topk_logit = logit;
+  a.lse = lse;
+  a.B = B;
+  a.L = p->L;
+  a.K = p->K;
+  a.cap = p->cap;
+  a.t_draft = p->t_draft;
+  a.t_verify = p->d_t_verify;
+  a.token_ids = token_ids;
+  a.parent = parent;
+  a.depth = depth;
+  a.path_prob = path_prob;
+  a.n_star = n_star;
+  a.phi = phi;
+  a.theta = theta;
+  hipError_t e = caddtree::launch_expand(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "expand launch");
+  return CADDTREE_OK;
+}
+
+caddtree_status_t run_emit(const caddtree_plan* p, const int32_t* parent, const int32_t* depth,
+                           const int32_t* n_star, int64_t B, int32_t pos_offset, void* mask, int32_t* pos_ids,
+                           hipStream_t stream) {
+  caddtree::EmitArgs a;
+  a.parent = parent;
+  a.depth = depth;
+  a.n_star = n_star;
+  a.B = B;
+  a.cap = p->cap;
+  a.pos_offset = pos_offset;
+  a.mask_kind = p->mask;
+  a.mask = p->mask == CADDTREE_MASK_NONE ? nullptr : mask;
+  a.pos_ids = pos_ids;
+  if (a.mask == nullptr && a.pos_ids == nullptr) return CADDTREE_OK;
+  hipError_t e = caddtree::launch_emit(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "emit launch");
+  return CADDTREE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* caddtree_status_string(caddtree_status_t s) {
+  switch (s) {
+    case CADDTREE_OK: return "ok";
+    case CADDTREE_E_INVALID: return "invalid argument";
+    case CADDTREE_E_UNSUPPORTED: return "unsupported configuration";
+    case CADDTREE_E_COST: return "cost model rejected";
+    case CADDTREE_E_WORKSPACE: return "workspace too small or misaligned";
+    case CADDTREE_E_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* caddtree_last_error(void) { return g_last_error.c_str(); }
+
+caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_plan_t* plan_out) {
+  if (plan_out == nullptr) return fail(CADDTREE_E_INVALID, "plan_out is NULL");
+  *plan_out = nullptr;
+  if (cfg == nullptr) return fail(CADDTREE_E_INVALID, "cfg is NULL");
+  if (cfg->L < 1) return fail(CADDTREE_E_INVALID, "L = %d must be >= 1", cfg->L);
+  if (cfg->L > CADDTREE_MAX_L) return fail(CADDTREE_E_UNSUPPORTED, "L = %d exceeds %d", cfg->L, CADDTREE_MAX_L);
+  if (cfg->K < 1) return fail(CADDTREE_E_INVALID, "K = %d must be >= 1", cfg->K);
+  if (cfg->K > CADDTREE_MAX_K) return fail(CADDTREE_E_UNSUPPORTED, "K = %d exceeds %d", cfg->K, CADDTREE_MAX_K);
+  if (cfg->V < cfg->K) return fail(CADDTREE_E_INVALID, "V = %lld is smaller than K = %d", (long long)cfg->V, cfg->K);
+  if (cfg->V > (int64_t)INT32_MAX - 1)
+    return fail(CADDTREE_E_UNSUPPORTED, "V = %lld exceeds 2^31 - 2", (long long)cfg->V);
+  if (cfg->budget_cap < 0) return fail(CADDTREE_E_INVALID, "budget_cap = %d is negative", cfg->budget_cap);
+  if (cfg->budget_cap > CADDTREE_MAX_CAP)
+    return fail(CADDTREE_E_UNSUPPORTED, "budget_cap = %d exceeds %d", cfg->budget_cap, CADDTREE_MAX_CAP);
+  if (cfg->dtype != CADDTREE_F32 && cfg->dtype != CADDTREE_BF16)
+    return fail(CADDTREE_E_INVALID, "unknown dtype %d", (int)cfg->dtype);
+  if (cfg->mask != CADDTREE_MASK_NONE && cfg->mask != CADDTREE_MASK_U8 && cfg->mask != CADDTREE_MASK_BITS32)
+    return fail(CADDTREE_E_INVALID, "unknown mask kind %d", (int)cfg->mask);
+  if (cfg->flags & ~CADDTREE_ALLOW_NONCONVEX) return fail(CADDTREE_E_INVALID, "unknown flags 0x%x", cfg->flags);
+  if (!(cfg->t_draft > 0.0) || !std::isfinite(cfg->t_draft))
+    return fail(CADDTREE_E_COST, "t_draft = %g must be finite and > 0", cfg->t_draft);
+  if (cfg->t_verify_host == nullptr) return fail(CADDTREE_E_INVALID, "t_verify_host is NULL");
+  const int cap = cfg->budget_cap;
+  const double* tv = cfg->t_verify_host;
+  double scale = 0.0;
+  for (int n = 0; n <= cap; ++n) {
+    if (!std::isfinite(tv[n])) return fail(CADDTREE_E_COST, "C_v(%d) is not finite", n);
+    if (!(cfg->t_draft + tv[n] > 0.0)) return fail(CADDTREE_E_COST, "C_d + C_v(%d) <= 0", n);
+    scale = std::fmax(scale, std::fabs(tv[n]));
+  }
+  const double slack = 1e-12 * std::fmax(scale, cfg->t_draft);
+  for (int n = 1; n <= cap; ++n)
+    if (tv[n] - tv[n - 1] < -slack)
+      return fail(CADDTREE_E_COST, "C_v decreases between n = %d and %d", n - 1, n);
+  if (!(cfg->flags & CADDTREE_ALLOW_NONCONVEX))
+    for (int n = 2; n <= cap; ++n)
+      if ((tv[n] - tv[n - 1]) - (tv[n - 1] - tv[n - 2]) < -slack)
+        return fail(CADDTREE_E_COST, "C_v is not convex at n = %d (Assumption 1 needs convex cost)", n - 1);
+
+  caddtree_plan* p = new (std::nothrow) caddtree_plan();
+  if (p == nullptr) return fail(CADDTREE_E_INVALID, "out of host memory");
+  p->L = cfg->L;
+  p->V = cfg->V;
+  p->K = cfg->K;
+  p->cap = cap;
+  p->dtype = cfg->dtype;
+  p->mask = cfg->mask;
+  p->flags = cfg->flags;
+  p->t_draft = cfg->t_draft;
+  p->d_t_verify = nullptr;
+  p->k1_waves = 0;
+  if (const char* env = std::getenv("CADDTREE_K1_WAVES")) {
+    const int w = std::atoi(env);
+    if (w == 1 || w == 2 || w == 4 || w == 8 || w == 16) p->k1_waves = w;
+  }
+  hipError_t e = hipGetDevice(&p->device);
+  if (e != hipSuccess) { delete p; return hip_fail(e, "hipGetDevice"); }
+  e = hipMalloc(&p->d_t_verify, sizeof(double) * (size_t)(cap + 1));
+  if (e != hipSuccess) { delete p; return hip_fail(e, "hipMalloc(cost table)"); }
+  e = hipMemcpy(p->d_t_verify, tv, sizeof(double) * (size_t)(cap + 1), hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = caddtree::expand_prepare(p->L, p->K, p->cap);
+  if (e != hipSuccess) {
+    (void)hipFree(p->d_t_verify);
+    delete p;
+    return hip_fail(e, "plan setup");
+  }
+  *plan_out = p;
+  return ok();
+}
+
+void caddtree_plan_destroy(caddtree_plan_t p) {
+  if (p == nullptr) return;
+  if (p->d_t_verify) (void)hipFree(p->d_t_verify);
+  delete p;
+}
+
+size_t caddtree_workspace_bytes(caddtree_plan_t p, int64_t B) {
+  if (p == nullptr || B <= 0) return 0;
+  TopkBuffers tb;
+  return topk_workspace(p, B, nullptr, nullptr, &tb);
+}
+
+caddtree_status_t caddtree_reduce_topk(caddtree_plan_t p, const void* logits, int64_t B, int64_t row_stride,
+                                       int32_t* topk_ids, float* topk_logit, float* topk_lq, double* lse,
+                                       hipStream_t stream) {
+  caddtree_status_t st = check_plan(p);
+  if (st != CADDTREE_OK) return st;
+  if ((st = check_logits(p, logits, B, row_stride)) != CADDTREE_OK) return st;
+  if (B > 0 && (topk_ids == nullptr || topk_logit == nullptr || lse == nullptr))
+    return fail(CADDTREE_E_INVALID, "topk_ids, topk_logit and lse are required");
+  if (B == 0) return ok();
+  if ((st = run_reduce(p, logits, B, row_stride, topk_ids, topk_logit, topk_lq, lse, stream)) != CADDTREE_OK)
+    return st;
+  return ok();
+}
+
+caddtree_status_t caddtree_expand(caddtree_plan_t p, const int32_t* topk_ids, const float* topk_logit,
+                                  const double* lse, int64_t B, int32_t* token_ids, int32_t* parent,
+                                  int32_t* depth, float* path_prob, int32_t* n_star, float* phi, float* theta,
+                                  hipStream_t stream) {
+  caddtree_status_t st = check_plan(p);
+  if (st != CADDTREE_OK) return st;
+  if (B < 0) return fail(CADDTREE_E_INVALID, "B = %lld is negative", (long long)B);
+  if (B == 0) return ok();
+  if (topk_ids == nullptr || topk_logit == nullptr || lse == nullptr)
+    return fail(CADDTREE_E_INVALID, "topk_ids, topk_logit and lse are required");
+  if (token_ids == nullptr || parent == nullptr || depth == nullptr || n_star == nullptr)
+    return fail(CADDTREE_E_INVALID, "token_ids, parent, depth and n_star are required");
+  if (B > (int64_t)INT32_MAX) return fail(CADDTREE_E_UNSUPPORTED, "B exceeds 2^31 - 1");
+  if ((st = run_expand(p, topk_ids, topk_logit, lse, B, token_ids, parent, depth, path_prob, n_star, phi,
+                       theta, stream)) != CADDTREE_OK)
+    return st;
+  return ok();
+}
+
+caddtree_status_t caddtree_emit(caddtree_plan_t p, const int32_t* parent, const int32_t* depth,
+                                const int32_t* n_star, int64_t B, int32_t pos_offset, void* mask,
+                                int32_t* pos_ids, hipStream_t stream) {
+  caddtree_status_t st = check_plan(p);
+  if (st != CADDTREE_OK) return st;
+  if (B < 0) return fail(CADDTREE_E_INVALID, "B = %lld is negative", (long long)B);
+  if (B == 0) return ok();
+  if (B > (int64_t)UINT32_MAX / 2) return fail(CADDTREE_E_UNSUPPORTED, "B too large");
+  if (parent == nullptr || n_star == nullptr) return fail(CADDTREE_E_INVALID, "parent and n_star are required");
+  if (pos_ids != nullptr && depth == nullptr) return fail(CADDTREE_E_INVALID, "pos_ids needs depth");
+  if ((st = run_emit(p, parent, depth, n_star, B, pos_offset, mask, pos_ids, stream)) != CADDTREE_OK) return st;
+  return ok();
+}
+
+caddtree_status_t caddtree_build(caddtree_plan_t p, const void* logits, int64_t B, int64_t row_stride,
+                                 int32_t pos_offset, const caddtree_outputs_t* out, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
+  caddtree_status_t st = check_plan(p);
+  if (st != CADDTREE_OK) return st;
+  if ((st = check_logits(p, logits, B, row_stride)) != CADDTREE_OK) return st;
+  if (out == nullptr) return fail(CADDTREE_E_INVALID, "out is NULL");
+  if (B == 0) return ok();
+  if (out->token_ids == nullptr || out->parent == nullptr || out->depth == nullptr || out->n_star == nullptr)
+    return fail(CADDTREE_E_INVALID, "out->token_ids, parent, depth and n_star are required");
+  TopkBuffers tb;
+  const size_t need = topk_workspace(p, B, out, nullptr, &tb);
+  if (need > 0) {
+    if (workspace == nullptr) return fail(CADDTREE_E_WORKSPACE, "workspace is NULL, %zu bytes needed", need);
+    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+      return fail(CADDTREE_E_WORKSPACE, "workspace must be 256-byte aligned");
+    if (workspace_bytes < need)
+      return fail(CADDTREE_E_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, need);
+  }
+  topk_workspace(p, B, out, static_cast<char*>(workspace), &tb);
+  if ((st = run_reduce(p, logits, B, row_stride, tb.ids, tb.logit, out->topk_lq, tb.lse, stream)) != CADDTREE_OK)
+    return st;
+  if ((st = run_expand(p, tb.ids, tb.logit, tb.lse, B, out->token_ids, out->parent, out->depth, out->path_prob,
+                       out->n_star, out->phi, out->theta, stream)) != CADDTREE_OK)
+    return st;
+  if ((st = run_emit(p, out->parent, out->depth, out->n_star, B, pos_offset, out->mask, out->pos_ids, stream)) !=
+      CADDTREE_OK)
+    return st;
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,64 @@
+// Internal launch interface between the host library (api.cpp) and the three kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "caddtree.h"
+
+namespace caddtree {
+
+// Stage 1: vocabulary reduction + top-K, one workgroup of `waves_per_row`
+// wavefronts per logit row.
+struct ReduceArgs {
+  const void* logits;
+  int64_t rows;          // B * L
+  int64_t row_stride;    // elements
+  int32_t V;
+  int32_t K;
+  int32_t waves_per_row; // 1 .. 16
+  bool aligned;          // rows start on 16-byte boundaries
+  int32_t* ids;          // [rows, K]
+  float* logit;          // [rows, K]
+  float* lq;             // [rows, K] or nullptr
+  double* lse;           // [rows]
+};
+hipError_t launch_reduce_topk(const ReduceArgs& a, caddtree_dtype_t dtype, hipStream_t stream);
+int reduce_default_waves(int64_t rows, int32_t V, caddtree_dtype_t dtype);
+
+// Stage 2: best-first expansion with the greedy stop, one workgroup per round.
+struct ExpandArgs {
+  const int32_t* topk_ids;
+  const float* topk_logit;
+  const double* lse;
+  int64_t B;
+  int32_t L, K, cap;
+  double t_draft;
+  const double* t_verify;  // device, cap + 1
+  int32_t* token_ids;
+  int32_t* parent;
+  int32_t* depth;
+  float* path_prob;        // optional
+  int32_t* n_star;
+  float* phi;              // optional
+  float* theta;            // optional
+};
+size_t expand_lds_bytes(int32_t L, int32_t K, int32_t cap);
+hipError_t expand_prepare(int32_t L, int32_t K, int32_t cap);  // raises the dynamic-LDS limit once
+hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream);
+
+// Stage 3: mask and position ids.
+struct EmitArgs {
+  const int32_t* parent;
+  const int32_t* depth;
+  const int32_t* n_star;
+  int64_t B;
+  int32_t cap;
+  int32_t pos_offset;
+  caddtree_mask_t mask_kind;
+  void* mask;              // optional
+  int32_t* pos_ids;        // optional
+};
+hipError_t launch_emit(const EmitArgs& a, hipStream_t stream);
+
+}  // namespace caddtree

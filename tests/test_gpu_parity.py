@@ -1,0 +1,264 @@
+"""GPU parity: the HIP library against the oracle, element by element, on seeded inputs.
+
+Small cases (several tiles, ragged tails, every dtype / mask / special case) are
+compared on every round; the full-size workloads are run in the launch
+configuration the benchmark times and compared on sampled rounds, with
+properties that hold at any size checked on every round.  Rounds are drawn
+through the input guard (tests/_guard.py), so every floating-point decision of
+a compared round has a relative margin of at least 1e-6.
+"""
+
+import numpy as np
+import pytest
+
+import synth
+from tests import _guard
+from tests._parity import (check_tree_properties, compare_topk, compare_tree, host, make_plan, run_build, say,
+                           torch_logits)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm GPU"
+    import paper_2606_01813_amd._lib as L
+    L.lib()  # the HIP library must be built and loadable: no fallback
+    return torch
+
+
+def _parity_batch(cfg, rounds, pos_offset=0, pad=0, mask=None):
+    attempts, x, rs = _guard.guarded_batch(cfg, rounds, pos_offset=pos_offset)
+    say(f"[parity] {cfg.name} L={cfg.L} V={cfg.V} K={cfg.K} cap={cfg.cap} {cfg.dtype} mask={mask or cfg.mask} "
+        f"rounds={len(rounds)} pad={pad} redraws={sum(attempts.values())}")
+    plan = make_plan(cfg, mask=mask)
+    out = run_build(plan, torch_logits(cfg, x, pad=pad), pos_offset=pos_offset)
+    h = host(out)
+    worst = compare_topk(h, rs)
+    if (mask or cfg.mask) == cfg.mask:
+        compare_tree(h, rs, mask or cfg.mask, cfg.cap, pos_offset=pos_offset)
+    say(f"[parity]   ok; max |lse - oracle| = {worst:.2e}; n* = {[r.n_star for r in rs][:12]}")
+    return h, rs
+
+
+SMALL = [
+    # name, overrides
+    ("c0", dict()),
+    ("c0", dict(B=48)),
+    ("c0", dict(V=1000, L=3, K=3, cap=40, B=16)),                       # ragged tail, short rows
+    ("c0", dict(V=17, L=2, K=2, cap=10, B=16)),                         # V below one wave chunk
+    ("c0", dict(V=4099, L=5, K=5, cap=64, B=8, dtype="bf16", mask="bits")),
+    ("c1", dict(V=20000, B=8)),                                         # full L=16, K=8, cap 512
+    ("c1", dict(V=2500, B=8, L=7, K=16, mask="bits")),
+    ("c3", dict(V=30011, B=6)),                                         # temperature mix, packed mask
+    ("c4", dict(V=3000, B=4)),                                          # L=32, K=16, cap 4096, fp32
+    ("c4", dict(V=64, B=4, K=16, L=32)),                                # V = one fp32 chunk
+]
+
+
+@pytest.mark.parametrize("i", range(len(SMALL)))
+def test_small_parity(i):
+    name, kw = SMALL[i]
+    cfg = synth.get_config(name).replace(**kw)
+    _parity_batch(cfg, list(range(cfg.B)), pos_offset=3 * i)
+
+
+def test_unaligned_rows_use_the_guarded_path():
+    cfg = synth.get_config("c1").replace(V=3001, B=4)
+    _parity_batch(cfg, list(range(cfg.B)), pad=1)        # row stride V + 1: rows off 16-byte boundaries
+    cfg32 = synth.get_config("c0").replace(V=999, B=4)
+    _parity_batch(cfg32, list(range(cfg32.B)), pad=3)
+
+
+def test_dense_and_packed_masks_agree():
+    cfg = synth.get_config("c1").replace(V=5000, B=4)
+    h8, rs = _parity_batch(cfg, list(range(4)), mask="u8")
+    hb, _ = _parity_batch(cfg, list(range(4)), mask="bits")
+    for i, r in enumerate(rs):
+        n = r.n_star
+        words = hb["mask"][i, :n, :(n + 31) // 32].view(np.uint32)
+        unpacked = np.array([[(words[a, c // 32] >> (c % 32)) & 1 for c in range(n)] for a in range(n)])
+        assert np.array_equal(unpacked, h8["mask"][i, :n, :n])
+
+
+# ------------------------------------------------------------- stage-by-stage
+
+def _oracle_tables(cfg, rs):
+    import torch
+    ids = torch.tensor(np.stack([r.marg["ids"] for r in rs]).astype(np.int32), device="cuda")
+    logit = torch.tensor(np.stack([r.marg["logit"] for r in rs]).astype(np.float32), device="cuda")
+    lse = torch.tensor(np.stack([r.marg["lse"] for r in rs]), dtype=torch.float64, device="cuda")
+    return ids, logit, lse
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("c0", dict(B=32)),
+    ("c1", dict(V=4000, B=8)),
+    ("c3", dict(V=4000, B=8)),
+    ("s1", dict(V=1500, B=2)),                         # constant cost: grows to the 4096 cap
+    ("s2", dict(V=1500, B=3)),                         # cold marginals: deep trees
+    ("c4", dict(V=800, B=4, cost="const", cap=700)),   # heap sizes far past the LDS fast cases
+])
+def test_expand_stage_on_oracle_inputs(name, kw):
+    """Algorithm 1 alone, fed the oracle's own top-K table and fp64 normalisers: no guard needed."""
+    import torch
+    cfg = synth.get_config(name).replace(**kw)
+    xs = synth.draw_batch(cfg)
+    rs = [_guard.oracle_round(cfg, xs[b]) for b in range(cfg.B)]
+    say(f"[expand] {cfg.name} L={cfg.L} K={cfg.K} cap={cfg.cap} n*={[r.n_star for r in rs]}")
+    plan = make_plan(cfg)
+    out = plan.new_outputs(cfg.B)
+    ids, logit, lse = _oracle_tables(cfg, rs)
+    plan.expand(ids, logit, lse, out)
+    plan.emit(out, pos_offset=0)
+    torch.cuda.synchronize()
+    h = host(out)
+    compare_tree(h, rs, cfg.mask, cfg.cap, prob_rtol=1e-6)
+    for i, r in enumerate(rs):
+        assert np.array_equal(h["path_prob"][i, :r.n_star], r.tree.path_prob.astype(np.float32))
+
+
+def test_emit_stage_on_oracle_trees():
+    import torch
+    cfg = synth.get_config("s2").replace(V=1200, B=3)
+    xs = synth.draw_batch(cfg)
+    rs = [_guard.oracle_round(cfg, xs[b], pos_offset=11) for b in range(cfg.B)]
+    for mask in ("u8", "bits"):
+        plan = make_plan(cfg, mask=mask)
+        out = plan.new_outputs(cfg.B)
+        for i, r in enumerate(rs):
+            n = r.n_star
+            out.parent[i, :n] = torch.tensor(r.tree.parent, dtype=torch.int32)
+            out.depth[i, :n] = torch.tensor(r.tree.depth, dtype=torch.int32)
+            out.n_star[i] = n
+        say(f"[emit] mask={mask} n*={[r.n_star for r in rs]}")
+        plan.emit(out, pos_offset=11)
+        torch.cuda.synchronize()
+        h = host(out)
+        for i, r in enumerate(rs):
+            n = r.n_star
+            assert np.array_equal(h["pos_ids"][i, :n], r.tree.pos_ids)
+            ref = _guard.oracle.emit_mask(r.tree.parent, mask, cfg.cap)
+            if mask == "u8":
+                assert np.array_equal(h["mask"][i, :n, :n], ref)
+            else:
+                w = (n + 31) // 32
+                assert np.array_equal(h["mask"][i, :n, :w].view(np.uint32), ref[:, :w])
+
+
+# ------------------------------------------------------------- special cases
+
+def test_special_costs():
+    import torch
+    base = synth.get_config("c1").replace(V=3000, B=4, cap=64)
+    xs = synth.draw_batch(base)
+    lg = torch_logits(base, xs)
+    cases = {
+        "steep": (1.0 + 1e6 * np.arange(65.0), lambda n: n == 0),
+        "constant": (np.ones(65), lambda n: n == 64),
+    }
+    for name, (tv, expect) in cases.items():
+        plan = make_plan(base, t_verify=tv)
+        out = run_build(plan, lg)
+        h = host(out)
+        say(f"[special] {name} n*={h['n_star'].tolist()}")
+        assert all(expect(int(n)) for n in h["n_star"])
+        for i in range(base.B):
+            r = _guard.oracle.build_round(xs[i], base.dtype, base.K, base.t_draft, tv, base.cap, mask=base.mask)
+            compare_tree(h, [r], base.mask, base.cap, rounds=[i])
+
+
+def test_cap_zero_and_empty_batch():
+    import torch
+    cfg = synth.get_config("c0").replace(cap=0, B=2)
+    plan = make_plan(cfg)
+    xs = synth.draw_batch(cfg)
+    out = run_build(plan, torch_logits(cfg, xs))
+    assert out.n_star.cpu().tolist() == [0, 0]
+    th = out.theta.cpu().numpy()
+    assert np.allclose(th, 1.0 / (1.0 + synth.cost_table(cfg)[0]))
+    empty = torch.zeros((0, cfg.L, cfg.V), dtype=torch.float32, device="cuda")
+    out0 = plan.new_outputs(0)
+    plan.build(empty, out0, workspace=None)
+    torch.cuda.synchronize()
+
+
+def test_k1_chain_and_l1():
+    cfg = synth.get_config("c0").replace(K=1, cap=16, B=6, V=700)
+    _parity_batch(cfg, list(range(cfg.B)))
+    cfg = synth.get_config("c0").replace(L=1, K=16, cap=16, B=6, V=5000)
+    _parity_batch(cfg, list(range(cfg.B)))
+
+
+def test_bf16_ties():
+    """Heavily tied bf16 logits: top-K and expansion tie-breaks must match exactly."""
+    import torch
+    cfg = synth.get_config("c1").replace(V=6000, B=4, L=4, K=16, cap=200)
+    rng = np.random.default_rng(7)
+    x32 = (np.round(rng.standard_normal((cfg.B, cfg.L, cfg.V)) * 2) / 2).astype(np.float32)
+    xs = synth.bf16_bits_from_f32(x32)
+    rs = [_guard.oracle_round(cfg, xs[b]) for b in range(cfg.B)]
+    plan = make_plan(cfg)
+    out = run_build(plan, torch_logits(cfg, xs))
+    h = host(out)
+    compare_topk(h, rs)
+    # expansion on the oracle's normalisers is exact even with equal-probability nodes
+    out2 = plan.new_outputs(cfg.B)
+    ids, logit, lse = _oracle_tables(cfg, rs)
+    plan.expand(ids, logit, lse, out2)
+    plan.emit(out2)
+    torch.cuda.synchronize()
+    compare_tree(host(out2), rs, cfg.mask, cfg.cap)
+
+
+def test_determinism():
+    cfg = synth.get_config("c1").replace(V=40000, B=12)
+    xs = synth.draw_batch(cfg)
+    plan = make_plan(cfg)
+    lg = torch_logits(cfg, xs)
+    a = host(run_build(plan, lg))
+    b = host(run_build(plan, lg))
+    for k in a:
+        if a[k] is not None:
+            assert np.array_equal(a[k], b[k]), k
+
+
+# ------------------------------------------------------------- full-size workloads
+
+def _full_size(name, sample, workers=16):
+    cfg = synth.get_config(name)
+    attempts, _, rs = _guard.guarded_batch(cfg, sample)
+    say(f"[full] {name}: B={cfg.B} L={cfg.L} V={cfg.V} {cfg.dtype}; guarded sample {sample} "
+        f"redraws={sum(attempts.values())}")
+    xs = synth.draw_batch(cfg, attempts=attempts, workers=workers)
+    plan = make_plan(cfg)
+    lg = torch_logits(cfg, xs)
+    del xs
+    out = run_build(plan, lg)
+    h = host(out)
+    worst = compare_topk(h, rs, rounds=sample)
+    compare_tree(h, rs, cfg.mask, cfg.cap, rounds=sample)
+    for i in range(cfg.B):
+        check_tree_properties(h, cfg, i)
+    ns = h["n_star"]
+    say(f"[full] {name}: ok; max |lse diff| {worst:.2e}; n* mean {ns.mean():.1f} min {ns.min()} max {ns.max()}")
+
+
+def test_full_c1():
+    _full_size("c1", list(range(64)))
+
+
+def test_full_c2():
+    rng = np.random.default_rng(2)
+    _full_size("c2", sorted({0, 1, 1023, 512} | set(rng.choice(1024, 12, replace=False).tolist())))
+
+
+def test_full_c3():
+    rng = np.random.default_rng(3)
+    _full_size("c3", sorted({0, 255} | set(rng.choice(256, 10, replace=False).tolist())))
+
+
+def test_full_c4():
+    rng = np.random.default_rng(4)
+    _full_size("c4", sorted({0, 255} | set(rng.choice(256, 6, replace=False).tolist())))
