@@ -149,9 +149,19 @@ class Plan:
             raise TypeError(f"logits must be {want}, got {logits.dtype}")
         if logits.dim() != 3 or logits.shape[1] != self.L or logits.shape[2] < self.V:
             raise ValueError(f"logits must be [B, {self.L}, >= {self.V}], got {tuple(logits.shape)}")
-        if logits.stride(2) != 1 or logits.stride(0) != logits.stride(1) * self.L:
-            raise ValueError("logits rows must be evenly strided: [B, L, V] with a unit last stride")
-        return int(logits.shape[0]), int(logits.stride(1))
+        B, L = int(logits.shape[0]), int(logits.shape[1])
+        # row (b, i) must sit at (b * L + i) * row_stride; strides of size-1 dims are free
+        if L > 1:
+            rs = int(logits.stride(1))
+            ok = B == 1 or int(logits.stride(0)) == rs * L
+        else:
+            rs = int(logits.stride(0)) if B > 1 else int(logits.shape[2])
+            ok = True
+        if logits.shape[2] > 1 and logits.stride(2) != 1:
+            ok = False
+        if not ok or rs < self.V:
+            raise ValueError("logits rows must be evenly strided: [B, L, >=V] with a unit last stride")
+        return B, rs
 
     def build(self, logits, out: TreeOutputs, pos_offset: int = 0, workspace=None, stream=None) -> None:
         B, stride = self._logits(logits)
