@@ -21,6 +21,7 @@ struct caddtree_plan {
   uint32_t flags;
   double t_draft;
   double* d_t_verify;   // device copy, cap + 1 values
+  bool use_level;       // C_v(1) > C_v(0): the batched expansion applies
   int device;
   int k1_waves;         // 0 = automatic
 };
@@ -140,6 +141,7 @@ caddtree_status_t run_expand(const caddtree_plan* p, const int32_t* ids, const f
   a.n_star = n_star;
   a.phi = phi;
   a.theta = theta;
+  a.use_level = p->use_level;
   hipError_t e = caddtree::launch_expand(a, stream);
   if (e != hipSuccess) return hip_fail(e, "expand launch");
   return CADDTREE_OK;
@@ -232,6 +234,10 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
   p->flags = cfg->flags;
   p->t_draft = cfg->t_draft;
   p->d_t_verify = nullptr;
+  p->use_level = cap >= 1 && tv[1] > tv[0];
+  if (const char* env = std::getenv("CADDTREE_EXPAND")) {
+    if (std::strcmp(env, "serial") == 0) p->use_level = false;
+  }
   p->k1_waves = 0;
   if (const char* env = std::getenv("CADDTREE_K1_WAVES")) {
     const int w = std::atoi(env);

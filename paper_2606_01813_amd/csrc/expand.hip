@@ -2,6 +2,10 @@
 // with the greedy throughput stop -- and the breadth-first layout of the
 // result.  One workgroup (one 64-lane wavefront) per round.
 //
+// This is the serial form: one pop at a time, exactly as Algorithm 1 runs.
+// It serves every round whose cost model starts flat (c_1 = 0) and every
+// round that the batched form (expand_level.hip) hands back.
+//
 // Keys.  A node s = (s_1 .. s_d) (0-based ranks) has Lambda(s) = sum_{i<=d}
 // l_i^(s_i) (raw fp32 logits widened to fp64, summed in depth order) and log
 // prefix probability sigma(s) = min(Lambda(s) - A_d, sigma(parent)),
@@ -39,6 +43,7 @@
 #include <cmath>
 #include <type_traits>
 
+#include "expand_common.h"
 #include "internal.h"
 
 namespace caddtree {
@@ -49,24 +54,7 @@ constexpr int kSlots = 4;                  // register frontier capacity = 256 e
 constexpr int kRegCap = kSlots * kThreads;
 constexpr int kParallelLayoutMax = 512;
 
-// packed node word: parent index + 1 (13 bits), rank (4 bits), depth (6 bits)
-__device__ __forceinline__ uint32_t pack(int parent, int rank, int depth) {
-  return (uint32_t)(parent + 1) | ((uint32_t)rank << 13) | ((uint32_t)depth << 17);
-}
-__device__ __forceinline__ int m_parent(uint32_t m) { return (int)(m & 0x1FFFu) - 1; }
-__device__ __forceinline__ int m_rank(uint32_t m) { return (int)((m >> 13) & 0xFu); }
-__device__ __forceinline__ int m_depth(uint32_t m) { return (int)((m >> 17) & 0x3Fu); }
-
-// min(a, b) that returns a unless b < a (the first argument wins ties, e.g. +0 / -0)
-__device__ __forceinline__ double pmin(double a, double b) { return b < a ? b : a; }
-
-__device__ __forceinline__ double rl_d(double v, int l) {
-  const uint64_t u = (uint64_t)__double_as_longlong(v);
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, l);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l);
-  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
-}
-__device__ __forceinline__ uint32_t rl_u(uint32_t v, int l) { return (uint32_t)__builtin_amdgcn_readlane((int)v, l); }
+using namespace xp;
 
 // lane i <- lane i - 1 across the whole wave (lane 0 keeps its own value)
 __device__ __forceinline__ uint32_t wshr_u(uint32_t v) {
@@ -151,8 +139,6 @@ struct Heap {
 };
 
 // ---------------------------------------------------------------- LDS layout
-__host__ __device__ __forceinline__ size_t a16(size_t x) { return (x + 15) & ~(size_t)15; }
-
 // The union region holds, one at a time: the kept nodes' rank-tuple keys, the
 // overflow heap, and the serial layout's scratch.
 __host__ __device__ __forceinline__ size_t union_bytes(size_t ncap) {
@@ -211,9 +197,10 @@ expand_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict__ to
               const double* __restrict__ tv, int32_t* __restrict__ token_ids,
               int32_t* __restrict__ parent_out, int32_t* __restrict__ depth_out,
               float* __restrict__ path_prob, int32_t* __restrict__ n_star_out,
-              float* __restrict__ phi_out, float* __restrict__ theta_out) {
+              float* __restrict__ phi_out, float* __restrict__ theta_out, int only_flagged) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int b = blockIdx.x;
+  if (only_flagged && n_star_out[b] != -1) return;   // the batched kernel finished this round
   const int lane = threadIdx.x;
   const int LK = L * K;
   const Lds s = carve(smem, (size_t)LK, cap > 0 ? (size_t)cap : 1);
@@ -484,10 +471,16 @@ hipError_t expand_prepare(int32_t L, int32_t K, int32_t cap) {
 
 hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream) {
   if (a.B == 0) return hipSuccess;
+  int only_flagged = 0;
+  if (a.use_level) {
+    const hipError_t e = launch_expand_level(a, stream);
+    if (e != hipSuccess) return e;
+    only_flagged = 1;
+  }
   const size_t lds = expand_lds_bytes(a.L, a.K, a.cap);
   hipLaunchKernelGGL(expand_kernel, dim3((unsigned)a.B), dim3(kThreads), lds, stream,
                      a.topk_ids, a.topk_logit, a.lse, a.L, a.K, a.cap, a.t_draft, a.t_verify,
-                     a.token_ids, a.parent, a.depth, a.path_prob, a.n_star, a.phi, a.theta);
+                     a.token_ids, a.parent, a.depth, a.path_prob, a.n_star, a.phi, a.theta, only_flagged);
   return hipGetLastError();
 }
 

@@ -42,10 +42,13 @@ struct ExpandArgs {
   int32_t* n_star;
   float* phi;              // optional
   float* theta;            // optional
+  bool use_level;          // try the batched kernel first (cost with c_1 > 0)
 };
 size_t expand_lds_bytes(int32_t L, int32_t K, int32_t cap);
 hipError_t expand_prepare(int32_t L, int32_t K, int32_t cap);  // raises the dynamic-LDS limit once
 hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream);
+hipError_t launch_expand_level(const ExpandArgs& a, hipStream_t stream);
+size_t expand_level_lds_bytes(int32_t L, int32_t K, int32_t cap);
 
 // Stage 3: mask and position ids.
 struct EmitArgs {

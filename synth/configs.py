@@ -65,6 +65,7 @@ _COSTS: Dict[str, Callable[[np.ndarray], np.ndarray]] = {
     "c3": _piecewise_c3,
     "c4": _quad(0.001, 0.000005),
     "const": lambda n: np.ones_like(n, dtype=np.float64),
+    "tiny": lambda n: 1.0 + 1e-6 * n,          # almost flat: trees of hundreds of nodes
 }
 
 

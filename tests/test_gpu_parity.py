@@ -99,6 +99,7 @@ def _oracle_tables(cfg, rs):
     ("s1", dict(V=1500, B=2)),                         # constant cost: grows to the 4096 cap
     ("s2", dict(V=1500, B=3)),                         # cold marginals: deep trees
     ("c4", dict(V=800, B=4, cost="const", cap=700)),   # heap sizes far past the LDS fast cases
+    ("c4", dict(V=900, B=3, cost="tiny", cap=1500)),   # rising cost, trees too large for the batched kernel
 ])
 def test_expand_stage_on_oracle_inputs(name, kw):
     """Algorithm 1 alone, fed the oracle's own top-K table and fp64 normalisers: no guard needed."""
@@ -117,6 +118,32 @@ def test_expand_stage_on_oracle_inputs(name, kw):
     compare_tree(h, rs, cfg.mask, cfg.cap, prob_rtol=1e-6)
     for i, r in enumerate(rs):
         assert np.array_equal(h["path_prob"][i, :r.n_star], r.tree.path_prob.astype(np.float32))
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("c1", dict(V=3000, B=16)),
+    ("c4", dict(V=1200, B=6)),
+    ("s2", dict(V=1000, B=4)),
+    ("c4", dict(V=900, B=2, cost="tiny", cap=1200)),
+])
+def test_expand_paths_agree(name, kw, monkeypatch):
+    """The batched expansion and the serial one give bit-identical trees."""
+    import torch
+    cfg = synth.get_config(name).replace(**kw)
+    xs = synth.draw_batch(cfg)
+    lg = torch_logits(cfg, xs)
+    outs = {}
+    for mode in ("auto", "serial"):
+        if mode == "serial":
+            monkeypatch.setenv("CADDTREE_EXPAND", "serial")
+        else:
+            monkeypatch.delenv("CADDTREE_EXPAND", raising=False)
+        plan = make_plan(cfg)
+        outs[mode] = host(run_build(plan, lg))
+    say(f"[paths] {cfg.name} n*={outs['auto']['n_star'].tolist()[:8]}")
+    for k, v in outs["auto"].items():
+        if v is not None:
+            assert np.array_equal(v, outs["serial"][k]), k
 
 
 def test_emit_stage_on_oracle_trees():
