@@ -72,6 +72,22 @@ def cpu_baseline(cfg, xs, target_s: float, max_rounds: int):
                       f"+ Algorithm 1 + mask per round; input generation excluded)"}
 
 
+def copy_probe(mib: int) -> None:
+    """A plain device copy of known size (y = x * 1, fp32) for counter calibration: one launch reads and
+    writes mib MiB.  The source is never written and a larger buffer is written after allocating it, so
+    none of it sits in a cache when the copy runs."""
+    import torch
+    n = mib * (1 << 20) // 4
+    x = torch.empty(n, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    evict = torch.zeros(max(n // 2, 1 << 28), dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    del evict
+    torch.mul(x, 1.0, out=y)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4, "launches": 1}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -81,7 +97,12 @@ def main():
     ap.add_argument("--workers", type=int, default=synth.gen.default_workers())
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run a plain elementwise copy of this many MiB (counter calibration)")
     args = ap.parse_args()
+    if args.copy_probe_mib:
+        copy_probe(args.copy_probe_mib)
+        return
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the rounds are independent and this "
