@@ -32,12 +32,23 @@ namespace caddtree {
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kUnroll = 4;
+#ifndef CADDTREE_K1_UNROLL
+#define CADDTREE_K1_UNROLL 4
+#endif
+constexpr int kUnroll = CADDTREE_K1_UNROLL;   // 16-byte loads in flight per lane
 constexpr float kLog2eHi = 0x1.715476p+0f;     // log2(e) rounded to fp32
 constexpr float kLog2eLo = 0x1.4ae0c0p-26f;    // log2(e) - kLog2eHi, rounded to fp32
 constexpr double kLog2eD = 0x1.71547652b82fep+0;
 constexpr double kLn2D = 0x1.62e42fefa39efp-1;
 constexpr float kNoExp = -1.0e30f;             // "no reference exponent yet"
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// streaming 16-byte load with the non-temporal hint: each byte of the logits is read once
+__device__ __forceinline__ uint4 stream_load(const uint4* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 template <typename T> struct Vec;
 template <> struct Vec<float> { static constexpr int n = 4; };
@@ -204,7 +215,7 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
     if (c + kUnroll <= cfull) {
       uint4 q[kUnroll];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) q[u] = p4[((c + u) * CH + lane * VEC) / VEC];
+      for (int u = 0; u < kUnroll; ++u) q[u] = stream_load(p4 + ((c + u) * CH + lane * VEC) / VEC);
       float x[kUnroll][VEC];
       float g = -INFINITY;
 #pragma unroll
@@ -229,7 +240,7 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
     for (; c + kUnroll <= cfull; c += kUnroll) {
       uint4 q[kUnroll];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) q[u] = p4[((c + u) * CH + lane * VEC) / VEC];
+      for (int u = 0; u < kUnroll; ++u) q[u] = stream_load(p4 + ((c + u) * CH + lane * VEC) / VEC);
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         float x[VEC];
@@ -239,7 +250,7 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
     }
     for (; c < cfull; ++c) {
       float x[VEC];
-      unpack(p4[(c * CH + lane * VEC) / VEC], x);
+      unpack(stream_load(p4 + (c * CH + lane * VEC) / VEC), x);
       chunk_full<VEC>(s, x, c * CH, K);
     }
   }
