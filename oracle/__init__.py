@@ -18,6 +18,9 @@ Contents
                position ids (Sec. 3.3).
 ``pipeline``   one round end to end, and the decision margins used by the
                input guard.
+``cost``       context-aware verification cost: linear interpolation between
+               cost tables profiled on a grid of context lengths (Sec. 4.6,
+               eq. cv-interp).
 
 Precision: fp64 throughout (bf16 and fp32 logits are widened exactly).
 """
@@ -26,10 +29,12 @@ from .vocab import widen, log_normalizer, top_k, marginals
 from .alg1 import expand, Expansion
 from .layout import canonical_order, emit_mask, TreeOut
 from .pipeline import build_round, RoundResult, decision_margins
+from .cost import context_cost
 
 __all__ = [
     "widen", "log_normalizer", "top_k", "marginals",
     "expand", "Expansion",
     "canonical_order", "emit_mask", "TreeOut",
     "build_round", "RoundResult", "decision_margins",
+    "context_cost",
 ]
