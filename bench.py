@@ -7,6 +7,11 @@ ids), with the logits already resident in HBM.  Prints ONE JSON line.
 
     python bench.py [--steps K] [--warmup W] [--workload c2]
 
+Other workloads (``--workload``): c1, c3, c4, the stress cases s1, s2, the
+context-aware cost variants c1x, c2x (one context length per round, nine cost
+tables, Sec. 4.6) and the fixed-budget (DDTree) variants c1f16, c1f128,
+c1f1024, c2f128, c2f1024.
+
 Default workload c2: 1024 rounds x L=16 x V=151936 bf16 logits, K=8, cap 512,
 C_d = 1, C_v(n) = 1 + 0.002 n + 0.00002 n^2 (the HBM-saturating batch of the
 L=16 / V=151936 / bf16 rounds/sec metric).  Inputs are the seeded synthetic
@@ -59,10 +64,16 @@ def cpu_baseline(cfg, xs, target_s: float, max_rounds: int):
     """The oracle (test infrastructure), one core, on a bounded sample of the same rounds."""
     import oracle
     tv = synth.cost_table(cfg)
+    if cfg.ctx:
+        grid, tables = synth.ctx_tables(cfg)
+        ell = synth.ctx_lengths(cfg, cfg.B)
     t0 = time.perf_counter()
     n = 0
     while n < min(max_rounds, xs.shape[0]):
-        oracle.build_round(xs[n], cfg.dtype, cfg.K, cfg.t_draft, tv, cfg.cap, mask=cfg.mask)
+        if cfg.ctx:
+            tv = oracle.context_cost(tables, grid, int(ell[n]))
+        oracle.build_round(xs[n], cfg.dtype, cfg.K, cfg.t_draft, tv, cfg.cap, mask=cfg.mask,
+                           budget=cfg.cap if cfg.fixed else None)
         n += 1
         if time.perf_counter() - t0 >= target_s:
             break
@@ -132,15 +143,21 @@ def main():
     else:
         logits = torch.from_numpy(xs).to(dev)
     del xs
-    plan = Plan(L=cfg.L, V=cfg.V, K=cfg.K, cap=cfg.cap, t_draft=cfg.t_draft, t_verify=synth.cost_table(cfg),
-                dtype=cfg.dtype, mask=cfg.mask)
+    cost_kw = dict(t_verify=synth.cost_table(cfg))
+    ctx = None
+    if cfg.ctx:
+        grid, tables = synth.ctx_tables(cfg)
+        cost_kw = dict(t_verify=tables, ctx_grid=grid)
+        ctx = torch.from_numpy(synth.ctx_lengths(cfg, cfg.B)).to(dev)
+    plan = Plan(L=cfg.L, V=cfg.V, K=cfg.K, cap=cfg.cap, t_draft=cfg.t_draft, dtype=cfg.dtype, mask=cfg.mask,
+                fixed_budget=cfg.fixed, **cost_kw)
     B = cfg.B
     out = plan.new_outputs(B)
     ws = plan.new_workspace(B)
     stream = torch.cuda.current_stream()
 
     def step():
-        plan.build(logits, out, pos_offset=0, workspace=ws, stream=stream)
+        plan.build(logits, out, pos_offset=0, workspace=ws, stream=stream, ctx_len=ctx)
 
     for _ in range(args.warmup):
         step()
@@ -163,7 +180,7 @@ def main():
         e[0].record(stream)
         plan.reduce_topk(logits, topk.topk_ids, topk.topk_logit, topk.lse, topk.topk_lq, stream=stream)
         e[1].record(stream)
-        plan.expand(topk.topk_ids, topk.topk_logit, topk.lse, topk, stream=stream)
+        plan.expand(topk.topk_ids, topk.topk_logit, topk.lse, topk, stream=stream, ctx_len=ctx)
         e[2].record(stream)
         plan.emit(topk, pos_offset=0, stream=stream)
         e[3].record(stream)
@@ -192,7 +209,9 @@ def main():
         "dtype": "f32+f64",
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: {B} rounds x L={cfg.L} x V={cfg.V} {cfg.dtype} logits, K={cfg.K}, "
-                               f"cap {cfg.cap}, mask {cfg.mask}",
+                               f"cap {cfg.cap}, mask {cfg.mask}"
+                               + (", context-aware cost (9 tables)" if cfg.ctx else "")
+                               + (", fixed budget" if cfg.fixed else ""),
                    "rounds": B, "L": cfg.L, "V": cfg.V, "logits_dtype": cfg.dtype, "K": cfg.K, "cap": cfg.cap,
                    "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",

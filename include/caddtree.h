@@ -18,7 +18,8 @@
  * Conventions shared by every entry point:
  *   - Device pointers are HIP device memory on the plan's device; host pointers
  *     are named *_host.  The caller owns every buffer; the library allocates
- *     nothing per call (a plan owns one small device copy of its cost table).
+ *     nothing per call (a plan owns one small device copy of its cost tables
+ *     and context-length grid).
  *   - All work is enqueued on the given stream and runs asynchronously; the
  *     return value reports argument validation (done synchronously, before
  *     anything is enqueued) and launch errors, not kernel completion.
@@ -55,6 +56,7 @@ extern "C" {
 #define CADDTREE_MAX_L 32
 #define CADDTREE_MAX_K 16
 #define CADDTREE_MAX_CAP 4096
+#define CADDTREE_MAX_CTX 64     /* context-length grid points */
 
 typedef enum {
   CADDTREE_OK = 0,
@@ -78,6 +80,10 @@ typedef enum { CADDTREE_MASK_NONE = 0, CADDTREE_MASK_U8 = 1, CADDTREE_MASK_BITS3
 /* flags */
 #define CADDTREE_ALLOW_NONCONVEX 1u  /* accept a C_v that is non-decreasing but not convex (Assumption 1
                                         may then fail: the greedy stop is still taken, optimality is not claimed) */
+#define CADDTREE_FIXED_BUDGET 2u     /* fixed-budget mode (the DDTree construction, Sec. 3.4): no stop rule;
+                                        every round keeps the top min(budget_cap, sum_d K^d) nodes by prefix
+                                        probability, in the same order and layout.  phi and theta are still
+                                        reported, theta from the plan's cost model at that size. */
 
 typedef struct caddtree_plan* caddtree_plan_t;   /* opaque, immutable after creation */
 
@@ -89,12 +95,18 @@ typedef struct {
   int32_t budget_cap;        /* maximum nodes per tree, 0 .. CADDTREE_MAX_CAP */
   caddtree_dtype_t dtype;    /* logits element type */
   caddtree_mask_t mask;      /* mask format written by caddtree_build / caddtree_emit */
-  uint32_t flags;            /* CADDTREE_ALLOW_NONCONVEX or 0 */
+  uint32_t flags;            /* CADDTREE_ALLOW_NONCONVEX | CADDTREE_FIXED_BUDGET, or 0 */
   double t_draft;            /* C_d > 0, drafting cost of one round (Sec. 4.2) */
-  const double* t_verify_host; /* HOST array of budget_cap + 1 values C_v(0 .. cap): verification
-                                  cost of a tree of n nodes (Sec. 4.2, Sec. 4.6).  Must be finite,
+  const double* t_verify_host; /* HOST array of max(n_ctx, 1) x (budget_cap + 1) values: row j is
+                                  C_v(0 .. cap; L_j), the verification cost of a tree of n nodes at
+                                  context length L_j (Sec. 4.2, Sec. 4.6).  Every row must be finite,
                                   non-decreasing and convex in n (Cor. 3) up to a relative rounding
                                   slack of 1e-12; copied at plan creation. */
+  int32_t n_ctx;             /* J, context-length grid points: 0 or 1 = one cost table and no context
+                                dependence (ctx_len is then ignored); 2 .. CADDTREE_MAX_CTX = one table
+                                per grid point, interpolated per round (Sec. 4.6, eq. cv-interp) */
+  const int64_t* ctx_grid_host; /* HOST, J context lengths 0 <= L_0 < L_1 < ... < L_{J-1} <= 2^53
+                                   (used when J >= 2); copied at plan creation */
 } caddtree_config_t;
 
 /* Validates cfg, copies the cost table to the current device and returns a plan.
@@ -136,12 +148,20 @@ typedef struct {
   double* lse;
 } caddtree_outputs_t;
 
+/* Context length of each round (plans with J >= 2 cost tables).  ctx_len is a
+ * DEVICE int64 array [B].  A round at context length l with L_j <= l < L_{j+1}
+ * uses C_v(n; l) = (1 - a) C_v(n; L_j) + a C_v(n; L_{j+1}), a = (l - L_j) /
+ * (L_{j+1} - L_j) (eq. cv-interp), each product and the sum rounded
+ * separately in fp64; l <= L_0 uses the L_0 table and l >= L_{J-1} the
+ * L_{J-1} table (no extrapolation, which could break convexity).  NULL is an
+ * error for such plans and is allowed otherwise. */
+
 /* The whole hot path for B rounds: reduce + top-K, expansion, emission.
  * logits: DEVICE [B, L, row_stride] of the plan's dtype; B >= 0 (0 is a no-op).
  * workspace: DEVICE, >= caddtree_workspace_bytes(plan, B) bytes, 256-byte aligned
  * (may be NULL when every top-K output pointer is given). */
 caddtree_status_t caddtree_build(caddtree_plan_t plan, const void* logits, int64_t B, int64_t row_stride,
-                                 int32_t pos_offset, const caddtree_outputs_t* out,
+                                 int32_t pos_offset, const int64_t* ctx_len, const caddtree_outputs_t* out,
                                  void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Stage 1 (Sec. 3.2): per (round, position) row, LSE in fp64 and the top-K by
@@ -151,10 +171,11 @@ caddtree_status_t caddtree_reduce_topk(caddtree_plan_t plan, const void* logits,
                                        hipStream_t stream);
 
 /* Stage 2 (Algorithm 1): best-first expansion with the greedy stop, tree in canonical order.
- * Inputs: topk_ids, topk_logit [B, L, K], lse [B, L] (DEVICE).  token_ids,
- * parent, depth, n_star required; path_prob, phi, theta optional. */
+ * Inputs: topk_ids, topk_logit [B, L, K], lse [B, L] (DEVICE); ctx_len as for
+ * caddtree_build.  token_ids, parent, depth, n_star required; path_prob, phi,
+ * theta optional. */
 caddtree_status_t caddtree_expand(caddtree_plan_t plan, const int32_t* topk_ids, const float* topk_logit,
-                                  const double* lse, int64_t B,
+                                  const double* lse, int64_t B, const int64_t* ctx_len,
                                   int32_t* token_ids, int32_t* parent, int32_t* depth, float* path_prob,
                                   int32_t* n_star, float* phi, float* theta, hipStream_t stream);
 

@@ -11,6 +11,11 @@ loads on first use); calls need the built library and a gfx950 device.
     out = plan.new_outputs(B)                 # torch tensors on the current device
     ws = plan.new_workspace(B)
     plan.build(logits, out, workspace=ws)      # logits: [B, L, >=V] bf16 tensor
+
+Context-aware cost (Sec. 4.6): pass ``t_verify`` as [J, cap + 1] tables with
+``ctx_grid`` (J increasing context lengths) and give ``ctx_len`` (int64 [B],
+on the device) to ``build`` / ``expand``.  ``fixed_budget=True`` selects the
+fixed-budget (DDTree) construction: the top ``cap`` nodes, no stop rule.
 """
 
 from __future__ import annotations
@@ -22,9 +27,9 @@ from typing import Optional
 import numpy as np
 
 from . import _lib
-from ._lib import CaddtreeError, MAX_CAP, MAX_K, MAX_L
+from ._lib import CaddtreeError, MAX_CAP, MAX_CTX, MAX_K, MAX_L
 
-__all__ = ["Plan", "TreeOutputs", "CaddtreeError", "MAX_L", "MAX_K", "MAX_CAP"]
+__all__ = ["Plan", "TreeOutputs", "CaddtreeError", "MAX_L", "MAX_K", "MAX_CAP", "MAX_CTX"]
 
 
 def _torch():
@@ -71,20 +76,33 @@ class Plan:
     """An immutable CaDDTree plan (shape limits, dtype, mask format, cost model)."""
 
     def __init__(self, L: int, V: int, K: int, cap: int, t_draft: float, t_verify,
-                 dtype: str = "bf16", mask: str = "u8", allow_nonconvex: bool = False):
+                 dtype: str = "bf16", mask: str = "u8", allow_nonconvex: bool = False,
+                 ctx_grid=None, fixed_budget: bool = False):
         self.L, self.V, self.K, self.cap = int(L), int(V), int(K), int(cap)
         self.dtype, self.mask = dtype, mask
         if dtype not in _lib.DTYPES:
             raise ValueError(f"dtype must be one of {sorted(_lib.DTYPES)}")
         if mask not in _lib.MASKS:
             raise ValueError(f"mask must be one of {sorted(_lib.MASKS)}")
-        tv = np.ascontiguousarray(np.asarray(t_verify, dtype=np.float64))
-        if tv.ndim != 1 or tv.shape[0] < self.cap + 1:
-            raise ValueError(f"t_verify needs cap + 1 = {self.cap + 1} values")
-        self._tv = tv
+        tv = np.asarray(t_verify, dtype=np.float64)
+        if ctx_grid is None:
+            if tv.ndim != 1 or tv.shape[0] < self.cap + 1:
+                raise ValueError(f"t_verify needs cap + 1 = {self.cap + 1} values")
+            tv = np.ascontiguousarray(tv[: self.cap + 1])
+            grid = np.zeros(1, dtype=np.int64)
+            n_ctx = 1
+        else:
+            grid = np.ascontiguousarray(np.asarray(ctx_grid, dtype=np.int64))
+            n_ctx = int(grid.shape[0])
+            if tv.ndim != 2 or tv.shape[0] != n_ctx or tv.shape[1] < self.cap + 1:
+                raise ValueError(f"t_verify needs [len(ctx_grid), cap + 1] = [{n_ctx}, {self.cap + 1}] values")
+            tv = np.ascontiguousarray(tv[:, : self.cap + 1])
+        self._tv, self._grid, self.n_ctx = tv, grid, n_ctx
+        self.fixed_budget = bool(fixed_budget)
+        flags = (_lib.ALLOW_NONCONVEX if allow_nonconvex else 0) | (_lib.FIXED_BUDGET if fixed_budget else 0)
         cfg = _lib.Config(self.L, self.V, self.K, self.cap, _lib.DTYPES[dtype], _lib.MASKS[mask],
-                          _lib.ALLOW_NONCONVEX if allow_nonconvex else 0, float(t_draft),
-                          tv.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+                          flags, float(t_draft), tv.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                          n_ctx, grid.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)))
         self._lib = _lib.lib()
         h = ctypes.c_void_p()
         _lib.check(self._lib.caddtree_plan_create(ctypes.byref(cfg), ctypes.byref(h)))
@@ -163,13 +181,23 @@ class Plan:
             raise ValueError("logits rows must be evenly strided: [B, L, >=V] with a unit last stride")
         return B, rs
 
-    def build(self, logits, out: TreeOutputs, pos_offset: int = 0, workspace=None, stream=None) -> None:
+    def _ctx(self, ctx_len, B: int) -> Optional[int]:
+        if ctx_len is None:
+            return None
+        torch = _torch()
+        if ctx_len.dtype != torch.int64 or tuple(ctx_len.shape) != (B,) or not ctx_len.is_contiguous():
+            raise ValueError(f"ctx_len must be a contiguous int64 tensor of shape ({B},)")
+        return _ptr(ctx_len)
+
+    def build(self, logits, out: TreeOutputs, pos_offset: int = 0, workspace=None, stream=None,
+              ctx_len=None) -> None:
         B, stride = self._logits(logits)
         ws_ptr = _ptr(workspace)
         ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
         st = out.as_struct()
-        _lib.check(self._lib.caddtree_build(self._h, _ptr(logits), B, stride, int(pos_offset), ctypes.byref(st),
-                                            ws_ptr, ws_bytes, _stream(stream, logits.device)))
+        _lib.check(self._lib.caddtree_build(self._h, _ptr(logits), B, stride, int(pos_offset),
+                                            self._ctx(ctx_len, B), ctypes.byref(st), ws_ptr, ws_bytes,
+                                            _stream(stream, logits.device)))
 
     def reduce_topk(self, logits, topk_ids, topk_logit, lse, topk_lq=None, stream=None) -> None:
         B, stride = self._logits(logits)
@@ -177,10 +205,10 @@ class Plan:
                                                   _ptr(topk_logit), _ptr(topk_lq), _ptr(lse),
                                                   _stream(stream, logits.device)))
 
-    def expand(self, topk_ids, topk_logit, lse, out: TreeOutputs, stream=None) -> None:
+    def expand(self, topk_ids, topk_logit, lse, out: TreeOutputs, stream=None, ctx_len=None) -> None:
         B = int(topk_ids.shape[0])
         _lib.check(self._lib.caddtree_expand(self._h, _ptr(topk_ids), _ptr(topk_logit), _ptr(lse), B,
-                                             _ptr(out.token_ids), _ptr(out.parent), _ptr(out.depth),
+                                             self._ctx(ctx_len, B), _ptr(out.token_ids), _ptr(out.parent), _ptr(out.depth),
                                              _ptr(out.path_prob), _ptr(out.n_star), _ptr(out.phi),
                                              _ptr(out.theta), _stream(stream, topk_ids.device)))
 

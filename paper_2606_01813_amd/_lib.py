@@ -12,7 +12,8 @@ OK, E_INVALID, E_UNSUPPORTED, E_COST, E_WORKSPACE, E_HIP = range(6)
 DTYPES = {"f32": 0, "bf16": 1}
 MASKS = {"none": 0, "u8": 1, "bits": 2}
 ALLOW_NONCONVEX = 1
-MAX_L, MAX_K, MAX_CAP = 32, 16, 4096
+FIXED_BUDGET = 2
+MAX_L, MAX_K, MAX_CAP, MAX_CTX = 32, 16, 4096, 64
 
 
 class CaddtreeError(RuntimeError):
@@ -32,6 +33,8 @@ class Config(ctypes.Structure):
         ("flags", ctypes.c_uint32),
         ("t_draft", ctypes.c_double),
         ("t_verify_host", ctypes.POINTER(ctypes.c_double)),
+        ("n_ctx", ctypes.c_int32),
+        ("ctx_grid_host", ctypes.POINTER(ctypes.c_int64)),
     ]
 
 
@@ -59,11 +62,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.caddtree_plan_destroy.restype = None
     lib.caddtree_workspace_bytes.argtypes = [vp, i64]
     lib.caddtree_workspace_bytes.restype = sz
-    lib.caddtree_build.argtypes = [vp, vp, i64, i64, i32, ctypes.POINTER(Outputs), vp, sz, vp]
+    lib.caddtree_build.argtypes = [vp, vp, i64, i64, i32, vp, ctypes.POINTER(Outputs), vp, sz, vp]
     lib.caddtree_build.restype = ctypes.c_int
     lib.caddtree_reduce_topk.argtypes = [vp, vp, i64, i64, vp, vp, vp, vp, vp]
     lib.caddtree_reduce_topk.restype = ctypes.c_int
-    lib.caddtree_expand.argtypes = [vp, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.caddtree_expand.argtypes = [vp, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.caddtree_expand.restype = ctypes.c_int
     lib.caddtree_emit.argtypes = [vp, vp, vp, vp, i64, i32, vp, vp, vp]
     lib.caddtree_emit.restype = ctypes.c_int

@@ -20,8 +20,10 @@ struct caddtree_plan {
   caddtree_mask_t mask;
   uint32_t flags;
   double t_draft;
-  double* d_t_verify;   // device copy, cap + 1 values
-  bool use_level;       // C_v(1) > C_v(0): the batched expansion applies
+  int32_t n_ctx;        // cost tables: 1, or one per context-length grid point
+  double* d_t_verify;   // device copy, n_ctx x (cap + 1) values
+  int64_t* d_ctx_grid;  // device copy of the grid (n_ctx >= 2), else NULL
+  bool use_level;       // the batched expansion applies (see plan_create)
   int device;
   int k1_waves;         // 0 = automatic
 };
@@ -121,9 +123,16 @@ caddtree_status_t run_reduce(const caddtree_plan* p, const void* logits, int64_t
   return CADDTREE_OK;
 }
 
+caddtree_status_t check_ctx(const caddtree_plan* p, const int64_t* ctx_len) {
+  if (p->n_ctx >= 2 && ctx_len == nullptr)
+    return fail(CADDTREE_E_INVALID, "ctx_len is required: the plan has %d context-length cost tables", p->n_ctx);
+  return CADDTREE_OK;
+}
+
 caddtree_status_t run_expand(const caddtree_plan* p, const int32_t* ids, const float* logit, const double* lse,
-                             int64_t B, int32_t* token_ids, int32_t* parent, int32_t* depth, float* path_prob,
-                             int32_t* n_star, float* phi, float* theta, hipStream_t stream) {
+                             int64_t B, const int64_t* ctx_len, int32_t* token_ids, int32_t* parent,
+                             int32_t* depth, float* path_prob, int32_t* n_star, float* phi, float* theta,
+                             hipStream_t stream) {
   caddtree::ExpandArgs a;
   a.topk_ids = ids;
   a.topk_logit = logit;
@@ -132,8 +141,12 @@ caddtree_status_t run_expand(const caddtree_plan* p, const int32_t* ids, const f
   a.L = p->L;
   a.K = p->K;
   a.cap = p->cap;
-  a.t_draft = p->t_draft;
-  a.t_verify = p->d_t_verify;
+  a.cost.tv = p->d_t_verify;
+  a.cost.grid = p->d_ctx_grid;
+  a.cost.ctx_len = ctx_len;
+  a.cost.J = p->n_ctx;
+  a.cost.stride = p->cap + 1;
+  a.cost.t_draft = p->t_draft;
   a.token_ids = token_ids;
   a.parent = parent;
   a.depth = depth;
@@ -142,6 +155,7 @@ caddtree_status_t run_expand(const caddtree_plan* p, const int32_t* ids, const f
   a.phi = phi;
   a.theta = theta;
   a.use_level = p->use_level;
+  a.fixed_budget = (p->flags & CADDTREE_FIXED_BUDGET) != 0;
   hipError_t e = caddtree::launch_expand(a, stream);
   if (e != hipSuccess) return hip_fail(e, "expand launch");
   return CADDTREE_OK;
@@ -202,26 +216,46 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
     return fail(CADDTREE_E_INVALID, "unknown dtype %d", (int)cfg->dtype);
   if (cfg->mask != CADDTREE_MASK_NONE && cfg->mask != CADDTREE_MASK_U8 && cfg->mask != CADDTREE_MASK_BITS32)
     return fail(CADDTREE_E_INVALID, "unknown mask kind %d", (int)cfg->mask);
-  if (cfg->flags & ~CADDTREE_ALLOW_NONCONVEX) return fail(CADDTREE_E_INVALID, "unknown flags 0x%x", cfg->flags);
+  if (cfg->flags & ~(CADDTREE_ALLOW_NONCONVEX | CADDTREE_FIXED_BUDGET))
+    return fail(CADDTREE_E_INVALID, "unknown flags 0x%x", cfg->flags);
   if (!(cfg->t_draft > 0.0) || !std::isfinite(cfg->t_draft))
     return fail(CADDTREE_E_COST, "t_draft = %g must be finite and > 0", cfg->t_draft);
   if (cfg->t_verify_host == nullptr) return fail(CADDTREE_E_INVALID, "t_verify_host is NULL");
-  const int cap = cfg->budget_cap;
-  const double* tv = cfg->t_verify_host;
-  double scale = 0.0;
-  for (int n = 0; n <= cap; ++n) {
-    if (!std::isfinite(tv[n])) return fail(CADDTREE_E_COST, "C_v(%d) is not finite", n);
-    if (!(cfg->t_draft + tv[n] > 0.0)) return fail(CADDTREE_E_COST, "C_d + C_v(%d) <= 0", n);
-    scale = std::fmax(scale, std::fabs(tv[n]));
+  if (cfg->n_ctx < 0) return fail(CADDTREE_E_INVALID, "n_ctx = %d is negative", cfg->n_ctx);
+  if (cfg->n_ctx > CADDTREE_MAX_CTX)
+    return fail(CADDTREE_E_UNSUPPORTED, "n_ctx = %d exceeds %d", cfg->n_ctx, CADDTREE_MAX_CTX);
+  const int J = cfg->n_ctx < 1 ? 1 : cfg->n_ctx;
+  if (J >= 2) {
+    const int64_t* g = cfg->ctx_grid_host;
+    if (g == nullptr) return fail(CADDTREE_E_INVALID, "ctx_grid_host is NULL with n_ctx = %d", J);
+    for (int j = 0; j < J; ++j) {
+      if (g[j] < 0 || g[j] > ((int64_t)1 << 53))
+        return fail(CADDTREE_E_INVALID, "ctx_grid_host[%d] = %lld is outside [0, 2^53]", j, (long long)g[j]);
+      if (j > 0 && g[j] <= g[j - 1])
+        return fail(CADDTREE_E_INVALID, "ctx_grid_host is not strictly increasing at %d", j);
+    }
   }
-  const double slack = 1e-12 * std::fmax(scale, cfg->t_draft);
-  for (int n = 1; n <= cap; ++n)
-    if (tv[n] - tv[n - 1] < -slack)
-      return fail(CADDTREE_E_COST, "C_v decreases between n = %d and %d", n - 1, n);
-  if (!(cfg->flags & CADDTREE_ALLOW_NONCONVEX))
-    for (int n = 2; n <= cap; ++n)
-      if ((tv[n] - tv[n - 1]) - (tv[n - 1] - tv[n - 2]) < -slack)
-        return fail(CADDTREE_E_COST, "C_v is not convex at n = %d (Assumption 1 needs convex cost)", n - 1);
+  const int cap = cfg->budget_cap;
+  double min_c1 = INFINITY;
+  for (int j = 0; j < J; ++j) {
+    const double* tv = cfg->t_verify_host + (size_t)j * (size_t)(cap + 1);
+    double scale = 0.0;
+    for (int n = 0; n <= cap; ++n) {
+      if (!std::isfinite(tv[n])) return fail(CADDTREE_E_COST, "C_v(%d) of table %d is not finite", n, j);
+      if (!(cfg->t_draft + tv[n] > 0.0)) return fail(CADDTREE_E_COST, "C_d + C_v(%d) <= 0 in table %d", n, j);
+      scale = std::fmax(scale, std::fabs(tv[n]));
+    }
+    const double slack = 1e-12 * std::fmax(scale, cfg->t_draft);
+    for (int n = 1; n <= cap; ++n)
+      if (tv[n] - tv[n - 1] < -slack)
+        return fail(CADDTREE_E_COST, "C_v of table %d decreases between n = %d and %d", j, n - 1, n);
+    if (!(cfg->flags & CADDTREE_ALLOW_NONCONVEX))
+      for (int n = 2; n <= cap; ++n)
+        if ((tv[n] - tv[n - 1]) - (tv[n - 1] - tv[n - 2]) < -slack)
+          return fail(CADDTREE_E_COST, "C_v of table %d is not convex at n = %d (Assumption 1 needs convex cost)",
+                      j, n - 1);
+    if (cap >= 1) min_c1 = std::fmin(min_c1, tv[1] - tv[0]);
+  }
 
   caddtree_plan* p = new (std::nothrow) caddtree_plan();
   if (p == nullptr) return fail(CADDTREE_E_INVALID, "out of host memory");
@@ -233,8 +267,17 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
   p->mask = cfg->mask;
   p->flags = cfg->flags;
   p->t_draft = cfg->t_draft;
+  p->n_ctx = J;
   p->d_t_verify = nullptr;
-  p->use_level = cap >= 1 && tv[1] > tv[0];
+  p->d_ctx_grid = nullptr;
+  // The batched expansion needs a threshold search that settles within its LDS
+  // store: costs that rise from the first node on (C_v(1) > C_v(0) in every
+  // table), or a fixed budget of at most 128 nodes.  Flat-start costs keep
+  // theta rising for many nodes, and go to the serial kernel.
+  if (cfg->flags & CADDTREE_FIXED_BUDGET)
+    p->use_level = cap >= 1 && cap <= 128;
+  else
+    p->use_level = cap >= 1 && min_c1 > 0.0;
   if (const char* env = std::getenv("CADDTREE_EXPAND")) {
     if (std::strcmp(env, "serial") == 0) p->use_level = false;
   }
@@ -245,12 +288,19 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
   }
   hipError_t e = hipGetDevice(&p->device);
   if (e != hipSuccess) { delete p; return hip_fail(e, "hipGetDevice"); }
-  e = hipMalloc(&p->d_t_verify, sizeof(double) * (size_t)(cap + 1));
+  const size_t tv_bytes = sizeof(double) * (size_t)J * (size_t)(cap + 1);
+  e = hipMalloc(&p->d_t_verify, tv_bytes);
   if (e != hipSuccess) { delete p; return hip_fail(e, "hipMalloc(cost table)"); }
-  e = hipMemcpy(p->d_t_verify, tv, sizeof(double) * (size_t)(cap + 1), hipMemcpyHostToDevice);
+  e = hipMemcpy(p->d_t_verify, cfg->t_verify_host, tv_bytes, hipMemcpyHostToDevice);
+  if (e == hipSuccess && J >= 2) {
+    e = hipMalloc(&p->d_ctx_grid, sizeof(int64_t) * (size_t)J);
+    if (e == hipSuccess)
+      e = hipMemcpy(p->d_ctx_grid, cfg->ctx_grid_host, sizeof(int64_t) * (size_t)J, hipMemcpyHostToDevice);
+  }
   if (e == hipSuccess) e = caddtree::expand_prepare(p->L, p->K, p->cap);
   if (e != hipSuccess) {
     (void)hipFree(p->d_t_verify);
+    if (p->d_ctx_grid) (void)hipFree(p->d_ctx_grid);
     delete p;
     return hip_fail(e, "plan setup");
   }
@@ -261,6 +311,7 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
 void caddtree_plan_destroy(caddtree_plan_t p) {
   if (p == nullptr) return;
   if (p->d_t_verify) (void)hipFree(p->d_t_verify);
+  if (p->d_ctx_grid) (void)hipFree(p->d_ctx_grid);
   delete p;
 }
 
@@ -285,7 +336,8 @@ caddtree_status_t caddtree_reduce_topk(caddtree_plan_t p, const void* logits, in
 }
 
 caddtree_status_t caddtree_expand(caddtree_plan_t p, const int32_t* topk_ids, const float* topk_logit,
-                                  const double* lse, int64_t B, int32_t* token_ids, int32_t* parent,
+                                  const double* lse, int64_t B, const int64_t* ctx_len, int32_t* token_ids,
+                                  int32_t* parent,
                                   int32_t* depth, float* path_prob, int32_t* n_star, float* phi, float* theta,
                                   hipStream_t stream) {
   caddtree_status_t st = check_plan(p);
@@ -297,8 +349,9 @@ caddtree_status_t caddtree_expand(caddtree_plan_t p, const int32_t* topk_ids, co
   if (token_ids == nullptr || parent == nullptr || depth == nullptr || n_star == nullptr)
     return fail(CADDTREE_E_INVALID, "token_ids, parent, depth and n_star are required");
   if (B > (int64_t)INT32_MAX) return fail(CADDTREE_E_UNSUPPORTED, "B exceeds 2^31 - 1");
-  if ((st = run_expand(p, topk_ids, topk_logit, lse, B, token_ids, parent, depth, path_prob, n_star, phi,
-                       theta, stream)) != CADDTREE_OK)
+  if ((st = check_ctx(p, ctx_len)) != CADDTREE_OK) return st;
+  if ((st = run_expand(p, topk_ids, topk_logit, lse, B, ctx_len, token_ids, parent, depth, path_prob, n_star,
+                       phi, theta, stream)) != CADDTREE_OK)
     return st;
   return ok();
 }
@@ -318,8 +371,8 @@ caddtree_status_t caddtree_emit(caddtree_plan_t p, const int32_t* parent, const 
 }
 
 caddtree_status_t caddtree_build(caddtree_plan_t p, const void* logits, int64_t B, int64_t row_stride,
-                                 int32_t pos_offset, const caddtree_outputs_t* out, void* workspace,
-                                 size_t workspace_bytes, hipStream_t stream) {
+                                 int32_t pos_offset, const int64_t* ctx_len, const caddtree_outputs_t* out,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
   caddtree_status_t st = check_plan(p);
   if (st != CADDTREE_OK) return st;
   if ((st = check_logits(p, logits, B, row_stride)) != CADDTREE_OK) return st;
@@ -327,6 +380,8 @@ caddtree_status_t caddtree_build(caddtree_plan_t p, const void* logits, int64_t 
   if (B == 0) return ok();
   if (out->token_ids == nullptr || out->parent == nullptr || out->depth == nullptr || out->n_star == nullptr)
     return fail(CADDTREE_E_INVALID, "out->token_ids, parent, depth and n_star are required");
+  if (B > (int64_t)INT32_MAX) return fail(CADDTREE_E_UNSUPPORTED, "B exceeds 2^31 - 1");
+  if ((st = check_ctx(p, ctx_len)) != CADDTREE_OK) return st;
   TopkBuffers tb;
   const size_t need = topk_workspace(p, B, out, nullptr, &tb);
   if (need > 0) {
@@ -339,8 +394,8 @@ caddtree_status_t caddtree_build(caddtree_plan_t p, const void* logits, int64_t 
   topk_workspace(p, B, out, static_cast<char*>(workspace), &tb);
   if ((st = run_reduce(p, logits, B, row_stride, tb.ids, tb.logit, out->topk_lq, tb.lse, stream)) != CADDTREE_OK)
     return st;
-  if ((st = run_expand(p, tb.ids, tb.logit, tb.lse, B, out->token_ids, out->parent, out->depth, out->path_prob,
-                       out->n_star, out->phi, out->theta, stream)) != CADDTREE_OK)
+  if ((st = run_expand(p, tb.ids, tb.logit, tb.lse, B, ctx_len, out->token_ids, out->parent, out->depth,
+                       out->path_prob, out->n_star, out->phi, out->theta, stream)) != CADDTREE_OK)
     return st;
   if ((st = run_emit(p, out->parent, out->depth, out->n_star, B, pos_offset, out->mask, out->pos_ids, stream)) !=
       CADDTREE_OK)

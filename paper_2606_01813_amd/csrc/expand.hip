@@ -193,8 +193,8 @@ size_t lds_bytes(size_t LK, size_t ncap) {
 // ---------------------------------------------------------------- kernel
 __global__ void __launch_bounds__(kThreads)
 expand_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict__ topk_logit,
-              const double* __restrict__ lse, int L, int K, int cap, double t_draft,
-              const double* __restrict__ tv, int32_t* __restrict__ token_ids,
+              const double* __restrict__ lse, int L, int K, int cap, CostTables ct, int fixed,
+              int32_t* __restrict__ token_ids,
               int32_t* __restrict__ parent_out, int32_t* __restrict__ depth_out,
               float* __restrict__ path_prob, int32_t* __restrict__ n_star_out,
               float* __restrict__ phi_out, float* __restrict__ theta_out, int only_flagged) {
@@ -204,6 +204,7 @@ expand_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict__ to
   const int lane = threadIdx.x;
   const int LK = L * K;
   const Lds s = carve(smem, (size_t)LK, cap > 0 ? (size_t)cap : 1);
+  const RoundCost C = ct.round(b);
 
   for (int i = lane; i < LK; i += kThreads) {
     s.tl[i] = topk_logit[(int64_t)b * LK + i];
@@ -220,9 +221,9 @@ expand_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict__ to
     }
   }
   // the lanes hold C(64 k + 1 + lane) for the current block k and prefetch block k + 1
-  double cblk = lane + 1 <= cap ? t_draft + tv[lane + 1] : 1.0;
-  double cnxt = 64 + lane + 1 <= cap ? t_draft + tv[64 + lane + 1] : 1.0;
-  const double c0 = t_draft + tv[0];
+  double cblk = lane + 1 <= cap ? C(lane + 1) : 1.0;
+  double cnxt = 64 + lane + 1 <= cap ? C(64 + lane + 1) : 1.0;
+  const double c0 = C(0);
   __syncthreads();
 
   // register frontier: positions [0, f), ascending towards the next pop
@@ -297,7 +298,7 @@ expand_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict__ to
     const float raw_child = s.tl[(d < L ? d : d - 1) * K];
     const double delta = exp(sig);
     const double theta_new = (1.0 + phi + delta) / rl_d(cblk, n & 63);
-    if (theta_new <= theta_prev) return false;
+    if (!fixed && theta_new <= theta_prev) return false;
     --f;
     const double base_lam = p >= 0 ? raw_lam : 0.0;
     const double base_sig = p >= 0 ? raw_sig : 0.0;
@@ -308,7 +309,7 @@ expand_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict__ to
     if ((n & 63) == 0) {
       cblk = cnxt;
       const int idx = n + 64 + lane + 1;
-      cnxt = idx <= cap ? t_draft + tv[idx] : 1.0;
+      cnxt = idx <= cap ? C(idx) : 1.0;
     }
     if (lane == 0) {   // before the pushes: their tie-breaks may walk through this node
       s.slam[me] = lam; s.ssig[me] = sig; s.smeta[me] = meta;
@@ -341,13 +342,13 @@ expand_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict__ to
     __syncthreads();
     if (lane == 0) {
       const Heap H{s.tl, s.slam, s.smeta, s.hsig, s.hmeta, K};
-      double cnext = n < cap ? t_draft + tv[n + 1] : 0.0;
+      double cnext = n < cap ? C(n + 1) : 0.0;
       while (f > 0 && n < cap) {
         const double sig = s.hsig[0];
         const uint32_t meta = s.hmeta[0];
         const double delta = exp(sig);
         const double theta_new = (1.0 + phi + delta) / cnext;
-        if (theta_new <= theta_prev) break;
+        if (!fixed && theta_new <= theta_prev) break;
         const int p = m_parent(meta), r = m_rank(meta), d = m_depth(meta);
         const double base_lam = p >= 0 ? s.slam[p] : 0.0;
         const double base_sig = p >= 0 ? s.ssig[p] : 0.0;
@@ -356,7 +357,7 @@ expand_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict__ to
         phi += delta;
         theta_prev = theta_new;
         const int me = n++;
-        if (n < cap) cnext = t_draft + tv[n + 1];
+        if (n < cap) cnext = C(n + 1);
         bool has_child = d < L;
         double cs = 0.0;
         uint32_t cm = 0;
@@ -479,7 +480,7 @@ hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream) {
   }
   const size_t lds = expand_lds_bytes(a.L, a.K, a.cap);
   hipLaunchKernelGGL(expand_kernel, dim3((unsigned)a.B), dim3(kThreads), lds, stream,
-                     a.topk_ids, a.topk_logit, a.lse, a.L, a.K, a.cap, a.t_draft, a.t_verify,
+                     a.topk_ids, a.topk_logit, a.lse, a.L, a.K, a.cap, a.cost, a.fixed_budget ? 1 : 0,
                      a.token_ids, a.parent, a.depth, a.path_prob, a.n_star, a.phi, a.theta, only_flagged);
   return hipGetLastError();
 }

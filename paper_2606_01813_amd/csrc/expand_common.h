@@ -29,5 +29,52 @@ __device__ __forceinline__ uint32_t rl_u(uint32_t v, int l) { return (uint32_t)_
 
 __host__ __device__ __forceinline__ size_t a16(size_t x) { return (x + 15) & ~(size_t)15; }
 
+// Round cost C(n) = C_d + C_v(n; l) (Sec. 4.2).  With a context-length grid
+// L_0 < .. < L_{J-1} and one table C_v(.; L_j) per grid point (Sec. 4.6), a
+// round at context length l with L_j <= l < L_{j+1} uses the linear
+// interpolation of eq. cv-interp, alpha = (l - L_j) / (L_{j+1} - L_j); l at or
+// outside either end of the grid takes that end's table.  Each product and the
+// sum are rounded separately (no fused multiply-add), so the value does not
+// depend on the compiler's contraction choices.
+struct RoundCost {
+  const double* lo;   // C_v(.; L_j), cap + 1 values
+  const double* hi;   // C_v(.; L_{j+1}) (== lo when alpha == 0)
+  double alpha;
+  double t_draft;
+
+  __device__ __forceinline__ double operator()(int n) const {
+#pragma clang fp contract(off)
+    const double cv = (1.0 - alpha) * lo[n] + alpha * hi[n];
+    return t_draft + cv;
+  }
+};
+
+// The plan's cost tables as the kernels see them.
+struct CostTables {
+  const double* tv;        // [J, cap + 1]
+  const int64_t* grid;     // [J] strictly increasing context lengths (J >= 2), else unused
+  const int64_t* ctx_len;  // [B] context length of each round (J >= 2), else unused
+  int32_t J;
+  int32_t stride;          // cap + 1
+  double t_draft;
+
+  __device__ __forceinline__ RoundCost round(int64_t b) const {
+    RoundCost c{tv, tv, 0.0, t_draft};
+    if (J >= 2) {
+      const int64_t ell = ctx_len[b];
+      if (ell >= grid[J - 1]) {
+        c.lo = c.hi = tv + (int64_t)(J - 1) * stride;
+      } else if (ell > grid[0]) {
+        int j = 0;
+        while (grid[j + 1] <= ell) ++j;
+        c.lo = tv + (int64_t)j * stride;
+        c.hi = c.lo + stride;
+        c.alpha = (double)(ell - grid[j]) / (double)(grid[j + 1] - grid[j]);
+      }
+    }
+    return c;
+  }
+};
+
 }  // namespace xp
 }  // namespace caddtree

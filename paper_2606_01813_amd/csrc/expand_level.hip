@@ -105,8 +105,8 @@ __device__ Lds carve(unsigned char* smem, size_t LK, size_t W) {
 
 __global__ void __launch_bounds__(kW)
 expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict__ topk_logit,
-                    const double* __restrict__ lse, int L, int K, int cap, double t_draft,
-                    const double* __restrict__ tv, int32_t* __restrict__ token_ids,
+                    const double* __restrict__ lse, int L, int K, int cap, CostTables ct, int fixed,
+                    int32_t* __restrict__ token_ids,
                     int32_t* __restrict__ parent_out, int32_t* __restrict__ depth_out,
                     float* __restrict__ path_prob, int32_t* __restrict__ n_star_out,
                     float* __restrict__ phi_out, float* __restrict__ theta_out) {
@@ -116,12 +116,13 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   const int LK = L * K;
   const int W = (cap < kSCap ? cap : kSCap) + 2;
   const Lds s = carve(smem, (size_t)LK, (size_t)W);
+  const RoundCost C = ct.round(b);
 
   for (int i = lane; i < LK; i += kW) {
     s.tl[i] = topk_logit[(int64_t)b * LK + i];
     s.tid[i] = topk_ids[(int64_t)b * LK + i];
   }
-  for (int i = lane; i < W; i += kW) s.cw[i] = i <= cap ? t_draft + tv[i] : 1.0;
+  for (int i = lane; i < W; i += kW) s.cw[i] = i <= cap ? C(i) : 1.0;
   // lane d holds A_d = sum_{i<=d} LSE_i, summed in depth order (d = 0 .. L)
   const double lse_l = lane < L ? lse[(int64_t)b * L + lane] : 0.0;
   double Areg = 0.0;
@@ -138,7 +139,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   const double A1 = rl_d(Areg, 1);
   const double top = pmin(0.0 + (double)s.tl[0] - A1, 0.0);   // the first node to pop
   double tau = top - 3.0;
-  if (s.cw[1] - s.cw[0] > 0.0) {
+  if (!fixed && s.cw[1] - s.cw[0] > 0.0) {
     const int m = cap < 32 ? cap : 32;
     tau = log(2.0 * (s.cw[1] - s.cw[0]) / s.cw[m]) - 0.5;
   }
@@ -242,7 +243,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
     for (int k = lane; k < ns; k += kW) {
       if (k < cap) {
         const int m = k + 1;
-        const double c = m < W ? s.cw[m] : t_draft + tv[m];
+        const double c = m < W ? s.cw[m] : C(m);
         s.th[k] = (1.0 + s.P[k] + s.dsort[k]) / c;
       }
     }
@@ -251,7 +252,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
     for (int k0 = 0; k0 < ns; k0 += kW) {
       const int k = k0 + lane;
       bool stop = false;
-      if (k < ns) stop = k >= cap || s.th[k] <= (k == 0 ? theta0 : s.th[k - 1]);
+      if (k < ns) stop = k >= cap || (!fixed && s.th[k] <= (k == 0 ? theta0 : s.th[k - 1]));
       const unsigned long long ms = __ballot(stop);
       if (ms) { kk = k0 + __builtin_ctzll(ms); break; }
     }
@@ -311,7 +312,7 @@ size_t expand_level_lds_bytes(int32_t L, int32_t K, int32_t cap) {
 hipError_t launch_expand_level(const ExpandArgs& a, hipStream_t stream) {
   if (a.B == 0) return hipSuccess;
   hipLaunchKernelGGL(expand_level_kernel, dim3((unsigned)a.B), dim3(kW), expand_level_lds_bytes(a.L, a.K, a.cap),
-                     stream, a.topk_ids, a.topk_logit, a.lse, a.L, a.K, a.cap, a.t_draft, a.t_verify,
+                     stream, a.topk_ids, a.topk_logit, a.lse, a.L, a.K, a.cap, a.cost, a.fixed_budget ? 1 : 0,
                      a.token_ids, a.parent, a.depth, a.path_prob, a.n_star, a.phi, a.theta);
   return hipGetLastError();
 }

@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include "caddtree.h"
+#include "expand_common.h"
 
 namespace caddtree {
 
@@ -33,8 +34,7 @@ struct ExpandArgs {
   const double* lse;
   int64_t B;
   int32_t L, K, cap;
-  double t_draft;
-  const double* t_verify;  // device, cap + 1
+  xp::CostTables cost;     // device cost tables, context grid and per-round context lengths
   int32_t* token_ids;
   int32_t* parent;
   int32_t* depth;
@@ -42,7 +42,8 @@ struct ExpandArgs {
   int32_t* n_star;
   float* phi;              // optional
   float* theta;            // optional
-  bool use_level;          // try the batched kernel first (cost with c_1 > 0)
+  bool use_level;          // try the batched kernel first
+  bool fixed_budget;       // no stop rule: keep the top min(cap, #nodes) nodes (DDTree)
 };
 size_t expand_lds_bytes(int32_t L, int32_t K, int32_t cap);
 hipError_t expand_prepare(int32_t L, int32_t K, int32_t cap);  // raises the dynamic-LDS limit once

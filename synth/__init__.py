@@ -15,10 +15,10 @@ bf16 logits are carried as ``uint16`` bit patterns (round-to-nearest-even from
 fp32); fp32 logits as ``float32``.
 """
 
-from .configs import CONFIGS, STRESS, Config, get_config, cost_table
+from .configs import CONFIGS, STRESS, VARIANTS, Config, get_config, cost_table, ctx_tables, ctx_lengths
 from .gen import draw_round, draw_batch, bf16_bits_from_f32
 
 __all__ = [
-    "CONFIGS", "STRESS", "Config", "get_config", "cost_table",
+    "CONFIGS", "STRESS", "VARIANTS", "Config", "get_config", "cost_table", "ctx_tables", "ctx_lengths",
     "draw_round", "draw_batch", "bf16_bits_from_f32",
 ]

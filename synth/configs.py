@@ -1,10 +1,14 @@
 """Workload configurations: shapes, dtypes, generator recipe and cost tables.
 
-The five graded workloads (``c0`` .. ``c4``) and two ungraded stress workloads
-(``s1``, ``s2``).  Costs are in arbitrary units; the drafting cost is 1.0
+The five graded workloads (``c0`` .. ``c4``), two ungraded stress workloads
+(``s1``, ``s2``) and variants that exercise the context-aware cost and the
+fixed-budget mode.  Costs are in arbitrary units; the drafting cost is 1.0
 everywhere.  The verification cost is given as a table ``C_v(0..cap)``, the
 form in which the method consumes it (a profiled, convex, non-decreasing
 function of the node count; the paper's cost model, Sec. 4.2 and Sec. 4.6).
+
+Context-aware variants carry one table per point of a context-length grid
+(Sec. 4.6 profiles at 0, 1k, .., 8k tokens) and a context length per round.
 """
 
 from __future__ import annotations
@@ -31,6 +35,8 @@ class Config:
     mask: str         # "u8" (dense bytes) or "bits" (packed u32, LSB first)
     recipe: str       # "normal", "peak" or "peak_temp"
     seed: int
+    ctx: str = ""     # context-cost recipe (``ctx_tables``); "" = one table
+    fixed: bool = False   # fixed-budget mode: the top-``cap`` tree, no stop rule
 
     @property
     def elem_bytes(self) -> int:
@@ -104,10 +110,50 @@ STRESS: Dict[str, Config] = {
 }
 
 
+# Context grid of the cost profile (Sec. 4.6: 0, 1k, .., 8k tokens).
+CTX_GRID = tuple(1000 * j for j in range(9))
+
+
+def _ctx9(j: int, n: np.ndarray) -> np.ndarray:
+    # the base cost and the marginal cost per node both grow with the context
+    # (what Sec. 5.3 reports of the measured profiles); convex in n at every j
+    return (1.0 + 0.05 * j) + (0.002 + 0.0005 * j) * n + (0.00002 + 0.000002 * j) * n * n
+
+
+def ctx_tables(cfg: Config):
+    """(grid [J] int64, tables [J, cap + 1] float64) of a context-aware workload."""
+    if cfg.ctx != "ctx9":
+        raise KeyError(f"workload {cfg.name} has no context-cost recipe")
+    n = np.arange(cfg.cap + 1, dtype=np.float64)
+    return np.array(CTX_GRID, dtype=np.int64), np.stack([_ctx9(j, n) for j in range(len(CTX_GRID))])
+
+
+def ctx_lengths(cfg: Config, B: int) -> np.ndarray:
+    """Context length of each round, int64 [B]: uniform on [-500, 9500] (so both ends of the grid are
+    passed), with every 7th round placed exactly on a grid point."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(cfg.seed, spawn_key=(1 << 30,))))
+    ell = rng.integers(-500, 9501, size=B).astype(np.int64)
+    on = np.arange(B) % 7 == 0
+    ell[on] = np.array(CTX_GRID, dtype=np.int64)[(np.arange(B)[on] // 7) % len(CTX_GRID)]
+    return ell
+
+
+# Variants: c1 / c2 shapes with the context-aware cost, and the fixed-budget
+# (DDTree) construction at budgets from its grid {16, .., 1024} (Sec. 5.1).
+VARIANTS: Dict[str, Config] = {
+    "c1x": CONFIGS["c1"].replace(name="c1x", ctx="ctx9", seed=SEED_BASE + 21),
+    "c2x": CONFIGS["c2"].replace(name="c2x", ctx="ctx9", seed=SEED_BASE + 22),
+    "c1f16": CONFIGS["c1"].replace(name="c1f16", cap=16, fixed=True, seed=SEED_BASE + 31),
+    "c1f128": CONFIGS["c1"].replace(name="c1f128", cap=128, fixed=True, seed=SEED_BASE + 32),
+    "c1f1024": CONFIGS["c1"].replace(name="c1f1024", cap=1024, fixed=True, seed=SEED_BASE + 33),
+    "c2f128": CONFIGS["c2"].replace(name="c2f128", cap=128, fixed=True, seed=SEED_BASE + 34),
+    "c2f1024": CONFIGS["c2"].replace(name="c2f1024", cap=1024, fixed=True, seed=SEED_BASE + 35),
+}
+
+
 def get_config(name: str) -> Config:
     name = name.lower()
-    if name in CONFIGS:
-        return CONFIGS[name]
-    if name in STRESS:
-        return STRESS[name]
-    raise KeyError(f"unknown workload {name!r}; known: {sorted(CONFIGS) + sorted(STRESS)}")
+    for table in (CONFIGS, STRESS, VARIANTS):
+        if name in table:
+            return table[name]
+    raise KeyError(f"unknown workload {name!r}; known: {sorted(CONFIGS) + sorted(STRESS) + sorted(VARIANTS)}")

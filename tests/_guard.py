@@ -23,16 +23,37 @@ TAU = 1e-6
 MAX_ATTEMPTS = 20
 
 
-def oracle_round(cfg: synth.Config, x: np.ndarray, pos_offset: int = 0, mask=None):
-    return oracle.build_round(x, cfg.dtype, cfg.K, cfg.t_draft, synth.cost_table(cfg), cfg.cap,
-                              pos_offset=pos_offset, mask=mask or cfg.mask)
+_CTX_CACHE: Dict[Tuple[str, int], Tuple[np.ndarray, np.ndarray, np.ndarray]] = {}
+
+
+def ctx_inputs(cfg: synth.Config):
+    """(grid, tables, context length of every round of the full batch) of a context-aware workload."""
+    key = (cfg.name, cfg.B)
+    if key not in _CTX_CACHE:
+        grid, tables = synth.ctx_tables(cfg)
+        _CTX_CACHE[key] = (grid, tables, synth.ctx_lengths(cfg, cfg.B))
+    return _CTX_CACHE[key]
+
+
+def round_cost(cfg: synth.Config, b: int) -> np.ndarray:
+    """C_v(0..cap) of round b: the workload's table, or the oracle's interpolation at the round's context."""
+    if not cfg.ctx:
+        return synth.cost_table(cfg)
+    grid, tables, ell = ctx_inputs(cfg)
+    return oracle.context_cost(tables, grid, int(ell[b]))
+
+
+def oracle_round(cfg: synth.Config, x: np.ndarray, pos_offset: int = 0, mask=None, b: int = 0):
+    return oracle.build_round(x, cfg.dtype, cfg.K, cfg.t_draft, round_cost(cfg, b), cfg.cap,
+                              pos_offset=pos_offset, mask=mask or cfg.mask,
+                              budget=cfg.cap if cfg.fixed else None)
 
 
 def guarded_round(cfg: synth.Config, b: int, tau: float = TAU, pos_offset: int = 0):
     """(attempt, logits, oracle result) for round b, redrawn until its margins clear tau."""
     for a in range(MAX_ATTEMPTS):
         x = synth.draw_round(cfg, b, a)
-        r = oracle_round(cfg, x, pos_offset)
+        r = oracle_round(cfg, x, pos_offset, b=b)
         stop, gap = oracle.decision_margins(r.exp)
         if stop >= tau and gap >= tau:
             return a, x, r

@@ -43,18 +43,33 @@ def torch_logits(cfg: synth.Config, x: np.ndarray, device="cuda", pad: int = 0):
 
 
 def make_plan(cfg: synth.Config, mask=None, **kw):
+    """A plan for the workload: its cost table (or context tables and grid) and its budget mode."""
     from paper_2606_01813_amd import Plan
+    if cfg.ctx and "t_verify" not in kw:
+        grid, tables = synth.ctx_tables(cfg)
+        kw.update(t_verify=tables, ctx_grid=grid)
+    kw.setdefault("fixed_budget", cfg.fixed)
     return Plan(L=cfg.L, V=cfg.V, K=cfg.K, cap=cfg.cap, t_draft=cfg.t_draft,
                 t_verify=kw.pop("t_verify", synth.cost_table(cfg)), dtype=cfg.dtype,
                 mask=mask or cfg.mask, **kw)
 
 
-def run_build(plan, logits, pos_offset=0, topk=True):
+def ctx_tensor(cfg: synth.Config, rounds, device="cuda"):
+    """Device int64 context lengths of the given rounds of a context-aware workload (None otherwise)."""
+    if not cfg.ctx:
+        return None
+    import torch
+    from tests._guard import ctx_inputs
+    ell = ctx_inputs(cfg)[2]
+    return torch.tensor(np.asarray(ell)[list(rounds)], dtype=torch.int64, device=device)
+
+
+def run_build(plan, logits, pos_offset=0, topk=True, ctx_len=None):
     import torch
     B = logits.shape[0]
     out = plan.new_outputs(B, device=logits.device, topk=topk)
     ws = plan.new_workspace(B, device=logits.device)
-    plan.build(logits, out, pos_offset=pos_offset, workspace=ws)
+    plan.build(logits, out, pos_offset=pos_offset, workspace=ws, ctx_len=ctx_len)
     torch.cuda.synchronize()
     return out
 
@@ -110,7 +125,13 @@ def check_tree_properties(h, cfg: synth.Config, i: int, t_verify=None):
     """Properties every output round satisfies, whatever its inputs (any size)."""
     n = int(h["n_star"][i])
     assert 0 <= n <= cfg.cap
-    tv = synth.cost_table(cfg) if t_verify is None else t_verify
+    if cfg.fixed:
+        total = sum(cfg.K ** d for d in range(1, cfg.L + 1))
+        assert n == min(cfg.cap, total)
+    if t_verify is None:
+        from tests._guard import round_cost
+        t_verify = round_cost(cfg, i)
+    tv = t_verify
     par, dep, tok = h["parent"][i, :n], h["depth"][i, :n], h["token_ids"][i, :n]
     assert np.all(par < np.arange(n))
     assert np.all((dep >= 1) & (dep <= cfg.L))

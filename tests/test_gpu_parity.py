@@ -13,8 +13,8 @@ import pytest
 
 import synth
 from tests import _guard
-from tests._parity import (check_tree_properties, compare_topk, compare_tree, host, make_plan, run_build, say,
-                           torch_logits)
+from tests._parity import (check_tree_properties, compare_topk, compare_tree, ctx_tensor, host, make_plan,
+                           run_build, say, torch_logits)
 
 pytestmark = pytest.mark.gpu
 
@@ -33,7 +33,7 @@ def _parity_batch(cfg, rounds, pos_offset=0, pad=0, mask=None):
     say(f"[parity] {cfg.name} L={cfg.L} V={cfg.V} K={cfg.K} cap={cfg.cap} {cfg.dtype} mask={mask or cfg.mask} "
         f"rounds={len(rounds)} pad={pad} redraws={sum(attempts.values())}")
     plan = make_plan(cfg, mask=mask)
-    out = run_build(plan, torch_logits(cfg, x, pad=pad), pos_offset=pos_offset)
+    out = run_build(plan, torch_logits(cfg, x, pad=pad), pos_offset=pos_offset, ctx_len=ctx_tensor(cfg, rounds))
     h = host(out)
     worst = compare_topk(h, rs)
     if (mask or cfg.mask) == cfg.mask:
@@ -262,7 +262,7 @@ def _full_size(name, sample, workers=16):
     plan = make_plan(cfg)
     lg = torch_logits(cfg, xs)
     del xs
-    out = run_build(plan, lg)
+    out = run_build(plan, lg, ctx_len=ctx_tensor(cfg, range(cfg.B)))
     h = host(out)
     worst = compare_topk(h, rs, rounds=sample)
     compare_tree(h, rs, cfg.mask, cfg.cap, rounds=sample)
@@ -289,3 +289,146 @@ def test_full_c3():
 def test_full_c4():
     rng = np.random.default_rng(4)
     _full_size("c4", sorted({0, 255} | set(rng.choice(256, 6, replace=False).tolist())))
+
+
+# ------------------------------------------------------------- context-aware cost (Sec. 4.6)
+
+def test_ctx_parity_small():
+    """Per-round context lengths inside, on and outside the grid, interpolated per eq. cv-interp."""
+    cfg = synth.get_config("c1x").replace(V=20000, B=21)
+    h, rs = _parity_batch(cfg, list(range(cfg.B)))
+    ell = _guard.ctx_inputs(cfg)[2][: cfg.B]
+    say(f"[ctx] ell={ell.tolist()}")
+    assert (ell < 0).any() and (ell > 8000).any() and np.isin(ell, synth.configs.CTX_GRID).any()
+
+
+def test_ctx_on_grid_point_equals_single_table():
+    """A round sitting on grid point L_j uses exactly the table C_v(.; L_j)."""
+    import torch
+    cfg = synth.get_config("c1x").replace(V=5000, B=6)
+    grid, tables = synth.ctx_tables(cfg)
+    xs = synth.draw_batch(cfg)
+    lg = torch_logits(cfg, xs)
+    plan = make_plan(cfg)
+    for j in (0, 3, 8):
+        ctx = torch.full((cfg.B,), int(grid[j]), dtype=torch.int64, device="cuda")
+        a = host(run_build(plan, lg, ctx_len=ctx))
+        single = make_plan(cfg.replace(ctx=""), t_verify=tables[j])
+        b = host(run_build(single, lg))
+        say(f"[ctx] grid point {grid[j]}: n*={a['n_star'].tolist()}")
+        for k in a:
+            if a[k] is not None:
+                assert np.array_equal(a[k], b[k]), (j, k)
+
+
+def test_ctx_budget_shrinks_with_context():
+    """Costs that grow with the context give budgets that do not grow with it, on the same round
+    (the behaviour Sec. 5.3 reports; here each step of the grid raises C_v(n) for every n > 0 and the
+    marginal costs too)."""
+    import torch
+    cfg = synth.get_config("c1x").replace(V=8000, B=8)
+    xs = synth.draw_batch(cfg)
+    lg = torch_logits(cfg, xs)
+    plan = make_plan(cfg)
+    prev = None
+    for ell in (0, 1500, 4000, 6500, 8000):
+        ctx = torch.full((cfg.B,), ell, dtype=torch.int64, device="cuda")
+        ns = host(run_build(plan, lg, ctx_len=ctx))["n_star"]
+        say(f"[ctx] ell={ell} n*={ns.tolist()}")
+        if prev is not None:
+            assert np.all(ns <= prev)
+        prev = ns
+
+
+def test_ctx_len_required():
+    import torch
+    from paper_2606_01813_amd import CaddtreeError
+    cfg = synth.get_config("c1x").replace(V=3000, B=2)
+    plan = make_plan(cfg)
+    lg = torch_logits(cfg, synth.draw_batch(cfg))
+    out = plan.new_outputs(cfg.B)
+    with pytest.raises(CaddtreeError):
+        plan.build(lg, out, workspace=plan.new_workspace(cfg.B))
+    torch.cuda.synchronize()
+
+
+def test_ctx_expand_paths_agree(monkeypatch):
+    cfg = synth.get_config("c1x").replace(V=3000, B=21)
+    xs = synth.draw_batch(cfg)
+    lg = torch_logits(cfg, xs)
+    ctx = ctx_tensor(cfg, range(cfg.B))
+    outs = {}
+    for mode in ("auto", "serial"):
+        if mode == "serial":
+            monkeypatch.setenv("CADDTREE_EXPAND", "serial")
+        else:
+            monkeypatch.delenv("CADDTREE_EXPAND", raising=False)
+        outs[mode] = host(run_build(make_plan(cfg), lg, ctx_len=ctx))
+    for k, v in outs["auto"].items():
+        if v is not None:
+            assert np.array_equal(v, outs["serial"][k]), k
+
+
+def test_full_c1x():
+    _full_size("c1x", list(range(64)))
+
+
+def test_full_c2x():
+    rng = np.random.default_rng(22)
+    _full_size("c2x", sorted({0, 7, 1023} | set(rng.choice(1024, 10, replace=False).tolist())))
+
+
+# ------------------------------------------------------------- fixed budget (DDTree, Sec. 3.4)
+
+@pytest.mark.parametrize("name,kw", [
+    ("c1f16", dict(V=6000, B=8)),
+    ("c1f128", dict(V=6000, B=8)),              # the batched kernel's range
+    ("c1f1024", dict(V=3000, B=3)),             # serial kernel with the LDS heap
+    ("c0", dict(fixed=True, cap=32, B=8)),      # fp32, L=4, K=4: 32 of 340 nodes
+    ("c0", dict(fixed=True, L=2, K=3, cap=20, B=4, V=50)),   # 12 nodes < cap: the whole tree
+])
+def test_fixed_budget_parity(name, kw):
+    cfg = synth.get_config(name).replace(**kw)
+    h, rs = _parity_batch(cfg, list(range(cfg.B)))
+    for i in range(cfg.B):
+        check_tree_properties(h, cfg, i)
+
+
+def test_fixed_budget_paths_agree(monkeypatch):
+    cfg = synth.get_config("c1f128").replace(V=3000, B=16)
+    xs = synth.draw_batch(cfg)
+    lg = torch_logits(cfg, xs)
+    outs = {}
+    for mode in ("auto", "serial"):
+        if mode == "serial":
+            monkeypatch.setenv("CADDTREE_EXPAND", "serial")
+        else:
+            monkeypatch.delenv("CADDTREE_EXPAND", raising=False)
+        outs[mode] = host(run_build(make_plan(cfg), lg))
+    for k, v in outs["auto"].items():
+        if v is not None:
+            assert np.array_equal(v, outs["serial"][k]), k
+
+
+def test_fixed_budget_is_top_n_of_the_greedy_tree():
+    """The fixed-budget tree at n* of the greedy stop is the greedy tree itself (Prop. 1: T*_n nest)."""
+    cfg = synth.get_config("c1").replace(V=6000, B=8)
+    xs = synth.draw_batch(cfg)
+    lg = torch_logits(cfg, xs)
+    g = host(run_build(make_plan(cfg), lg))
+    for i in range(cfg.B):
+        n = int(g["n_star"][i])
+        f = host(run_build(make_plan(cfg.replace(cap=max(n, 1), fixed=True)), lg[i:i + 1]))
+        if n == 0:
+            continue
+        for k in ("token_ids", "parent", "depth"):
+            assert np.array_equal(f[k][0, :n], g[k][i, :n]), (i, k)
+
+
+def test_full_c2f128():
+    rng = np.random.default_rng(34)
+    _full_size("c2f128", sorted({0, 1023} | set(rng.choice(1024, 8, replace=False).tolist())))
+
+
+def test_full_c1f1024():
+    _full_size("c1f1024", [0, 17, 63])

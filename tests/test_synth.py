@@ -66,3 +66,13 @@ def test_cost_tables():
 def test_config_table(name):
     cfg = synth.get_config(name)
     assert cfg.K <= 16 and cfg.L <= 32 and cfg.cap <= 4096 and cfg.K <= cfg.V
+
+
+def test_ctx_lengths_prefix_stable():
+    """A smaller batch of a context-aware workload sees the same context lengths as the full batch."""
+    cfg = synth.get_config("c1x")
+    full = synth.ctx_lengths(cfg, cfg.B)
+    assert np.array_equal(synth.ctx_lengths(cfg, 21), full[:21])
+    grid, tables = synth.ctx_tables(cfg)
+    assert tables.shape == (len(grid), cfg.cap + 1)
+    assert np.all(np.diff(tables, axis=1) > 0) and np.all(np.diff(tables, 2, axis=1) > 0)
