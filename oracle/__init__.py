@@ -21,6 +21,10 @@ Contents
 ``cost``       context-aware verification cost: linear interpolation between
                cost tables profiled on a grid of context lengths (Sec. 4.6,
                eq. cv-interp).
+``accept``     synthetic acceptance: a target path drawn from the drafter's
+               factorised distribution, the accepted length under tree
+               verification (Sec. 3.3, eq. surrogate) and the throughput
+               sum (1 + alpha) / sum C (Sec. 4.2).
 
 Precision: fp64 throughout (bf16 and fp32 logits are widened exactly).
 """
@@ -30,11 +34,12 @@ from .alg1 import expand, Expansion
 from .layout import canonical_order, emit_mask, TreeOut
 from .pipeline import build_round, RoundResult, decision_margins
 from .cost import context_cost
+from . import accept
 
 __all__ = [
     "widen", "log_normalizer", "top_k", "marginals",
     "expand", "Expansion",
     "canonical_order", "emit_mask", "TreeOut",
     "build_round", "RoundResult", "decision_margins",
-    "context_cost",
+    "context_cost", "accept",
 ]
