@@ -185,6 +185,31 @@ caddtree_status_t caddtree_emit(caddtree_plan_t plan, const int32_t* parent, con
                                 const int32_t* n_star, int64_t B, int32_t pos_offset,
                                 void* mask, int32_t* pos_ids, hipStream_t stream);
 
+/* Synthetic acceptance (tree verification, Sec. 3.3) of B built trees against
+ * target continuations drawn from the drafter's factorised distribution
+ * (eq. factorized), under which the expected accepted length of a tree is
+ * Phi (eq. surrogate).  For a simulated throughput sum (1 + alpha) / sum C
+ * (Sec. 4.2) over many rounds.
+ *   topk_ids, topk_logit [B, L, K], lse [B, L]: DEVICE, as written by stage 1
+ *   token_ids, parent [B, tree_stride], n_star [B]: DEVICE, a tree as written
+ *       by caddtree_build / caddtree_expand (tree_stride = the budget cap of
+ *       the plan that built it; n_star is clamped to [0, tree_stride])
+ *   u [B, L]: DEVICE fp64 uniforms in [0, 1), owned by the caller (the random
+ *       numbers are inputs).  Position i draws rank r for the smallest r with
+ *       u_i < q^(0) + .. + q^(r), q^(k) = exp(l^(k) - LSE_i), the sum formed
+ *       left to right in fp64; u_i at or above the sum of all K draws a token
+ *       outside the top-K, which no node carries.
+ *   accept_len [B] int32 (required): the length of the longest drawn prefix
+ *       that is a path of the tree, 0 .. L.
+ *   round_cost [B] fp64 (optional): C_d + C_v(n_star; l) from THIS plan's cost
+ *       model (which may differ from the one that built the trees), NaN when
+ *       n_star lies outside [0, cap]; ctx_len as for caddtree_build. */
+caddtree_status_t caddtree_accept(caddtree_plan_t plan, const int32_t* topk_ids, const float* topk_logit,
+                                  const double* lse, int64_t B, const int32_t* token_ids, const int32_t* parent,
+                                  int32_t tree_stride, const int32_t* n_star, const double* u,
+                                  const int64_t* ctx_len, int32_t* accept_len, double* round_cost,
+                                  hipStream_t stream);
+
 const char* caddtree_status_string(caddtree_status_t status);
 const char* caddtree_last_error(void);
 

@@ -212,6 +212,21 @@ class Plan:
                                              _ptr(out.path_prob), _ptr(out.n_star), _ptr(out.phi),
                                              _ptr(out.theta), _stream(stream, topk_ids.device)))
 
+    def accept(self, topk: TreeOutputs, tree: TreeOutputs, u, accept_len, round_cost=None, ctx_len=None,
+               stream=None) -> None:
+        """Synthetic acceptance of ``tree`` (built from the top-K table in ``topk``) against target paths
+        drawn from the uniforms ``u`` (float64 [B, L]); writes ``accept_len`` (int32 [B]) and optionally
+        ``round_cost`` (float64 [B], this plan's C_d + C_v(n*))."""
+        torch = _torch()
+        B = int(tree.token_ids.shape[0])
+        if u.dtype != torch.float64 or tuple(u.shape) != (B, self.L) or not u.is_contiguous():
+            raise ValueError(f"u must be a contiguous float64 tensor of shape ({B}, {self.L})")
+        _lib.check(self._lib.caddtree_accept(self._h, _ptr(topk.topk_ids), _ptr(topk.topk_logit), _ptr(topk.lse),
+                                             B, _ptr(tree.token_ids), _ptr(tree.parent),
+                                             int(tree.token_ids.shape[1]), _ptr(tree.n_star), _ptr(u),
+                                             self._ctx(ctx_len, B), _ptr(accept_len), _ptr(round_cost),
+                                             _stream(stream, u.device)))
+
     def emit(self, out: TreeOutputs, pos_offset: int = 0, stream=None) -> None:
         B = int(out.parent.shape[0])
         _lib.check(self._lib.caddtree_emit(self._h, _ptr(out.parent), _ptr(out.depth), _ptr(out.n_star), B,

@@ -403,4 +403,46 @@ caddtree_status_t caddtree_build(caddtree_plan_t p, const void* logits, int64_t 
   return ok();
 }
 
+caddtree_status_t caddtree_accept(caddtree_plan_t p, const int32_t* topk_ids, const float* topk_logit,
+                                  const double* lse, int64_t B, const int32_t* token_ids, const int32_t* parent,
+                                  int32_t tree_stride, const int32_t* n_star, const double* u,
+                                  const int64_t* ctx_len, int32_t* accept_len, double* round_cost,
+                                  hipStream_t stream) {
+  caddtree_status_t st = check_plan(p);
+  if (st != CADDTREE_OK) return st;
+  if (B < 0) return fail(CADDTREE_E_INVALID, "B = %lld is negative", (long long)B);
+  if (tree_stride < 0) return fail(CADDTREE_E_INVALID, "tree_stride = %d is negative", tree_stride);
+  if (B == 0) return ok();
+  if (B > (int64_t)INT32_MAX) return fail(CADDTREE_E_UNSUPPORTED, "B exceeds 2^31 - 1");
+  if (topk_ids == nullptr || topk_logit == nullptr || lse == nullptr)
+    return fail(CADDTREE_E_INVALID, "topk_ids, topk_logit and lse are required");
+  if (token_ids == nullptr || parent == nullptr || n_star == nullptr || u == nullptr || accept_len == nullptr)
+    return fail(CADDTREE_E_INVALID, "token_ids, parent, n_star, u and accept_len are required");
+  if (round_cost != nullptr && (st = check_ctx(p, ctx_len)) != CADDTREE_OK) return st;
+  caddtree::AcceptArgs a;
+  a.topk_ids = topk_ids;
+  a.topk_logit = topk_logit;
+  a.lse = lse;
+  a.B = B;
+  a.L = p->L;
+  a.K = p->K;
+  a.token_ids = token_ids;
+  a.parent = parent;
+  a.tree_stride = tree_stride;
+  a.n_star = n_star;
+  a.u = u;
+  a.cost.tv = p->d_t_verify;
+  a.cost.grid = p->d_ctx_grid;
+  a.cost.ctx_len = ctx_len;
+  a.cost.J = p->n_ctx;
+  a.cost.stride = p->cap + 1;
+  a.cost.t_draft = p->t_draft;
+  a.cap = p->cap;
+  a.accept_len = accept_len;
+  a.round_cost = round_cost;
+  hipError_t e = caddtree::launch_accept(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "accept launch");
+  return ok();
+}
+
 }  // extern "C"

@@ -65,4 +65,23 @@ struct EmitArgs {
 };
 hipError_t launch_emit(const EmitArgs& a, hipStream_t stream);
 
+// Synthetic acceptance of built trees against drawn target paths.
+struct AcceptArgs {
+  const int32_t* topk_ids;
+  const float* topk_logit;
+  const double* lse;
+  int64_t B;
+  int32_t L, K;
+  const int32_t* token_ids;  // [B, tree_stride]
+  const int32_t* parent;     // [B, tree_stride]
+  int32_t tree_stride;
+  const int32_t* n_star;
+  const double* u;           // [B, L] uniforms in [0, 1)
+  xp::CostTables cost;
+  int32_t cap;               // the plan's cost tables cover n = 0 .. cap
+  int32_t* accept_len;
+  double* round_cost;        // optional
+};
+hipError_t launch_accept(const AcceptArgs& a, hipStream_t stream);
+
 }  // namespace caddtree

@@ -138,6 +138,13 @@ def ctx_lengths(cfg: Config, B: int) -> np.ndarray:
     return ell
 
 
+def accept_uniforms(cfg: Config, B: int, draw: int = 0) -> np.ndarray:
+    """Uniforms in [0, 1), float64 [B, L], for drawing target paths in the acceptance simulation; ``draw``
+    selects an independent stream (a redraw, or another sample of the same rounds)."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(cfg.seed, spawn_key=(1 << 29, draw))))
+    return rng.random((B, cfg.L))
+
+
 # Variants: c1 / c2 shapes with the context-aware cost, and the fixed-budget
 # (DDTree) construction at budgets from its grid {16, .., 1024} (Sec. 5.1).
 VARIANTS: Dict[str, Config] = {

@@ -70,3 +70,20 @@ def guarded_batch(cfg: synth.Config, rounds, tau: float = TAU, pos_offset: int =
         xs.append(x)
         rs.append(r)
     return attempts, np.stack(xs), rs
+
+
+def guarded_uniforms(cfg: synth.Config, rs, rounds, tau: float = TAU, max_draws: int = MAX_ATTEMPTS):
+    """Uniforms [len(rounds), L] for the acceptance draw of the given rounds (oracle results rs): each
+    round takes the first draw whose uniforms keep a relative distance of at least tau from every
+    cumulative boundary they are compared with."""
+    draws = [synth.accept_uniforms(cfg, max(rounds) + 1, k) for k in range(max_draws)]
+    out = np.empty((len(rounds), cfg.L))
+    for j, (b, r) in enumerate(zip(rounds, rs)):
+        for k in range(max_draws):
+            u = draws[k][b]
+            if oracle.accept.sample_margin(r.marg["logit"], r.marg["lse"], u) >= tau:
+                out[j] = u
+                break
+        else:
+            raise RuntimeError(f"round {b}: no acceptance draw clears the guard")
+    return out

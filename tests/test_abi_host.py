@@ -117,6 +117,8 @@ def test_null_arguments(lib):
     assert lib.caddtree_expand(None, None, None, None, 1, None, None, None, None, None, None, None, None,
                                None) == _lib.E_INVALID
     assert lib.caddtree_emit(None, None, None, None, 1, 0, None, None, None) == _lib.E_INVALID
+    assert lib.caddtree_accept(None, None, None, None, 1, None, None, 8, None, None, None, None, None,
+                               None) == _lib.E_INVALID
     assert lib.caddtree_workspace_bytes(None, 10) == 0
     lib.caddtree_plan_destroy(None)
 

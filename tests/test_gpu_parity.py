@@ -432,3 +432,88 @@ def test_full_c2f128():
 
 def test_full_c1f1024():
     _full_size("c1f1024", [0, 17, 63])
+
+
+# ------------------------------------------------------------- synthetic acceptance (Sec. 3.3, eq. surrogate)
+
+def _accept(plan, topk, tree, u, ctx=None):
+    import torch
+    B = int(tree.token_ids.shape[0])
+    al = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+    rc = torch.full((B,), -7.0, dtype=torch.float64, device="cuda")
+    plan.accept(topk, tree, torch.tensor(np.ascontiguousarray(u), dtype=torch.float64, device="cuda"), al, rc,
+                ctx_len=ctx)
+    torch.cuda.synchronize()
+    return al.cpu().numpy(), rc.cpu().numpy()
+
+
+def test_accept_stage_on_oracle_inputs():
+    """The oracle's own top-K tables and trees: the draw and the walk alone."""
+    import torch
+    cfg = synth.get_config("s2").replace(V=1500, B=6)
+    xs = synth.draw_batch(cfg)
+    rs = [_guard.oracle_round(cfg, xs[b]) for b in range(cfg.B)]
+    u = _guard.guarded_uniforms(cfg, rs, list(range(cfg.B)), tau=1e-9)
+    plan = make_plan(cfg)
+    topk = plan.new_outputs(cfg.B, topk=True)
+    ids, logit, lse = _oracle_tables(cfg, rs)
+    topk.topk_ids, topk.topk_logit, topk.lse = ids, logit, lse
+    tree = plan.new_outputs(cfg.B)
+    for i, r in enumerate(rs):
+        n = r.n_star
+        tree.token_ids[i, :n] = torch.tensor(r.tree.token_ids, dtype=torch.int32)
+        tree.parent[i, :n] = torch.tensor(r.tree.parent, dtype=torch.int32)
+        tree.n_star[i] = n
+    al, rc = _accept(plan, topk, tree, u)
+    want = [_guard.oracle.accept.simulate_round(r, u[i]) for i, r in enumerate(rs)]
+    say(f"[accept] s2 n*={[r.n_star for r in rs]} alpha={al.tolist()}")
+    assert al.tolist() == want
+    tv = synth.cost_table(cfg)
+    assert rc.tolist() == [_guard.oracle.accept.round_cost(cfg.t_draft, tv, r.n_star) for r in rs]
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("c1", dict(V=20000, B=16)),
+    ("c1x", dict(V=8000, B=14)),
+    ("c0", dict(B=40)),
+    ("c1f128", dict(V=5000, B=6)),
+])
+def test_accept_end_to_end(name, kw):
+    """Build on the GPU, then accept: alpha and the round cost equal the oracle's on guarded draws."""
+    cfg = synth.get_config(name).replace(**kw)
+    rounds = list(range(cfg.B))
+    attempts, x, rs = _guard.guarded_batch(cfg, rounds)
+    u = _guard.guarded_uniforms(cfg, rs, rounds)
+    plan = make_plan(cfg)
+    ctx = ctx_tensor(cfg, rounds)
+    out = run_build(plan, torch_logits(cfg, x), ctx_len=ctx)
+    al, rc = _accept(plan, out, out, u, ctx=ctx)
+    want = [_guard.oracle.accept.simulate_round(r, u[i]) for i, r in enumerate(rs)]
+    say(f"[accept] {name} alpha={al.tolist()[:16]}")
+    assert al.tolist() == want
+    costs = [_guard.oracle.accept.round_cost(cfg.t_draft, _guard.round_cost(cfg, b), r.n_star)
+             for b, r in zip(rounds, rs)]
+    assert rc.tolist() == costs
+
+
+def test_accept_mean_is_phi_full_c2():
+    """At full size: over 1024 rounds and 8 draws each, the mean accepted length matches the mean Phi
+    (eq. surrogate) within 4.5 standard errors."""
+    import torch
+    cfg = synth.get_config("c2")
+    xs = synth.draw_batch(cfg, workers=16)
+    lg = torch_logits(cfg, xs)
+    del xs
+    plan = make_plan(cfg)
+    out = run_build(plan, lg)
+    phi = out.phi.cpu().numpy().astype(np.float64)
+    alphas = []
+    for k in range(8):
+        al, rc = _accept(plan, out, out, synth.accept_uniforms(cfg, cfg.B, k))
+        assert np.all((al >= 0) & (al <= cfg.L))
+        alphas.append(al)
+    a = np.stack(alphas).astype(np.float64)
+    # per round: E[alpha] = Phi; the rounds' draws are independent
+    se = np.sqrt(a.var(axis=0, ddof=0).mean() / a.size + 1e-12)
+    say(f"[accept] c2 mean alpha {a.mean():.4f} mean phi {phi.mean():.4f} se {se:.4f}")
+    assert abs(a.mean() - phi.mean()) < 4.5 * max(se, 1e-3)
