@@ -12,6 +12,14 @@ context-aware cost variants c1x, c2x (one context length per round, nine cost
 tables, Sec. 4.6) and the fixed-budget (DDTree) variants c1f16, c1f128,
 c1f1024, c2f128, c2f1024.
 
+``--simulate`` runs the synthetic analogue of the paper's comparisons
+(Tab. 1-3) instead: trees from CaDDTree, from the fixed-budget construction
+at every budget of the DDTree grid {16, .., 1024}, from a constant C_v and
+from perturbed cost parameters, each verified against target paths drawn from
+the drafter's marginals (``caddtree_accept``) and charged under the nominal
+cost model; prints one JSON line with time per token (sum C / sum (1 +
+alpha), in units of C_d), mean accepted length and mean budget per variant.
+
 Default workload c2: 1024 rounds x L=16 x V=151936 bf16 logits, K=8, cap 512,
 C_d = 1, C_v(n) = 1 + 0.002 n + 0.00002 n^2 (the HBM-saturating batch of the
 L=16 / V=151936 / bf16 rounds/sec metric).  Inputs are the seeded synthetic
@@ -99,20 +107,87 @@ def copy_probe(mib: int) -> None:
     print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4, "launches": 1}), flush=True)
 
 
+DDTREE_GRID = (16, 32, 64, 128, 256, 512, 1024)
+
+
+def simulate(args) -> None:
+    """Simulated time per token of CaDDTree against the fixed-budget construction and cost ablations."""
+    import torch
+    from paper_2606_01813_amd import Plan
+    cfg = synth.get_config(args.workload or "s2")
+    assert not cfg.ctx and not cfg.fixed, "simulate takes a plain workload"
+    log(f"[simulate] generating {cfg.name}: {cfg.B} x {cfg.L} x {cfg.V} {cfg.dtype}")
+    xs = synth.draw_batch(cfg, workers=args.workers)
+    dev = torch.device("cuda:0")
+    if cfg.dtype == "bf16":
+        logits = torch.from_numpy(xs.view(np.int16)).to(dev).view(torch.bfloat16)
+    else:
+        logits = torch.from_numpy(xs).to(dev)
+    del xs
+    B = cfg.B
+    tv = synth.cost_table(cfg)
+    big = max(cfg.cap, max(DDTREE_GRID))
+    nominal = Plan(L=cfg.L, V=cfg.V, K=cfg.K, cap=big, t_draft=cfg.t_draft,
+                   t_verify=synth.cost_table(cfg.cost, big), dtype=cfg.dtype, mask="none")
+    us = [torch.from_numpy(synth.accept_uniforms(cfg, B, k)).to(dev) for k in range(args.draws)]
+
+    variants = [("caddtree", dict(cap=cfg.cap, t_draft=cfg.t_draft, t_verify=tv))]
+    variants += [(f"fixed_{n}", dict(cap=n, t_draft=cfg.t_draft, t_verify=synth.cost_table(cfg.cost, n),
+                                    fixed_budget=True)) for n in DDTREE_GRID]
+    flat = np.full(min(cfg.cap, 1024) + 1, tv[0])
+    variants += [("constant_cv", dict(cap=min(cfg.cap, 1024), t_draft=cfg.t_draft, t_verify=flat))]
+    variants += [("cd_x0.5", dict(cap=cfg.cap, t_draft=0.5 * cfg.t_draft, t_verify=tv)),
+                 ("cd_x2", dict(cap=cfg.cap, t_draft=2.0 * cfg.t_draft, t_verify=tv)),
+                 ("cv_x0.5", dict(cap=cfg.cap, t_draft=cfg.t_draft, t_verify=0.5 * tv)),
+                 ("cv_x2", dict(cap=cfg.cap, t_draft=cfg.t_draft, t_verify=2.0 * tv))]
+    rows = {}
+    for vname, kw in variants:
+        plan = Plan(L=cfg.L, V=cfg.V, K=cfg.K, dtype=cfg.dtype, mask="none", **kw)
+        out = plan.new_outputs(B, topk=True)
+        plan.build(logits, out, workspace=plan.new_workspace(B))
+        al = torch.empty(B, dtype=torch.int32, device=dev)
+        rc = torch.empty(B, dtype=torch.float64, device=dev)
+        tot_c = tot_t = tot_a = 0.0
+        for u in us:
+            nominal.accept(out, out, u, al, rc)
+            tot_c += float(rc.sum())
+            tot_t += float((al.to(torch.float64) + 1.0).sum())
+            tot_a += float(al.to(torch.float64).sum())
+        ns = out.n_star.to(torch.float64)
+        rows[vname] = {"time_per_token": tot_c / tot_t, "mean_accept": tot_a / (B * len(us)),
+                       "mean_n_star": float(ns.mean()), "std_n_star": float(ns.std()),
+                       "mean_phi": float(out.phi.to(torch.float64).mean())}
+        log(f"[simulate] {vname:12s} time/token {rows[vname]['time_per_token']:.4f} "
+            f"accept {rows[vname]['mean_accept']:.3f} n* {rows[vname]['mean_n_star']:.1f}")
+        plan.close()
+    best = min(DDTREE_GRID, key=lambda n: rows[f"fixed_{n}"]["time_per_token"])
+    line = {"simulate": cfg.name, "rounds": B, "draws": len(us),
+            "workload": f"{cfg.name}: {B} rounds x L={cfg.L} x V={cfg.V} {cfg.dtype}, K={cfg.K}, cap {cfg.cap}",
+            "cost_units": "C_d = 1", "variants": rows, "ddtree_oracle_budget": best,
+            "caddtree_over_ddtree_oracle": rows["caddtree"]["time_per_token"] / rows[f"fixed_{best}"]["time_per_token"]}
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="c2")
+    ap.add_argument("--workload", default=None, help="default c2 (s2 with --simulate)")
     ap.add_argument("--workers", type=int, default=synth.gen.default_workers())
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain elementwise copy of this many MiB (counter calibration)")
+    ap.add_argument("--simulate", action="store_true",
+                    help="synthetic analogue of the paper's comparisons (default workload s2)")
+    ap.add_argument("--draws", type=int, default=16, help="target-path draws per round for --simulate")
     args = ap.parse_args()
     if args.copy_probe_mib:
         copy_probe(args.copy_probe_mib)
+        return
+    if args.simulate:
+        simulate(args)
         return
 
     if args.gpus != 1:
@@ -120,7 +195,7 @@ def main():
               f"build has no multi-GPU path; run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
-    cfg = synth.get_config(args.workload)
+    cfg = synth.get_config(args.workload or "c2")
     log(f"[bench] generating {cfg.name}: {cfg.B} x {cfg.L} x {cfg.V} {cfg.dtype} ({cfg.batch_bytes / 1e9:.2f} GB) "
         f"with {args.workers} workers")
     t = time.perf_counter()
