@@ -25,6 +25,8 @@ Contents
                factorised distribution, the accepted length under tree
                verification (Sec. 3.3, eq. surrogate) and the throughput
                sum (1 + alpha) / sum C (Sec. 4.2).
+``costfit``    convex non-decreasing least-squares fit of a cost profile and the
+               cost table built from it (Sec. 4.6, eq. convex-reg).
 
 Precision: fp64 throughout (bf16 and fp32 logits are widened exactly).
 """
@@ -34,12 +36,12 @@ from .alg1 import expand, Expansion
 from .layout import canonical_order, emit_mask, TreeOut
 from .pipeline import build_round, RoundResult, decision_margins
 from .cost import context_cost
-from . import accept
+from . import accept, costfit
 
 __all__ = [
     "widen", "log_normalizer", "top_k", "marginals",
     "expand", "Expansion",
     "canonical_order", "emit_mask", "TreeOut",
     "build_round", "RoundResult", "decision_margins",
-    "context_cost", "accept",
+    "context_cost", "accept", "costfit",
 ]
