@@ -210,6 +210,22 @@ caddtree_status_t caddtree_accept(caddtree_plan_t plan, const int32_t* topk_ids,
                                   const int64_t* ctx_len, int32_t* accept_len, double* round_cost,
                                   hipStream_t stream);
 
+/* HOST only (no GPU, no stream): the offline cost model of Sec. 4.6.  Fits a
+ * verification-cost profile y_j measured at node counts x_j (x strictly
+ * increasing, all finite, 1 <= N <= 2^22) by the least-squares function that
+ * is convex and non-decreasing (eq. convex-reg): a piecewise-linear function
+ * whose breakpoints the data choose, solved exactly (active-set non-negative
+ * least squares on the slope changes).
+ *   fit_host [N] (optional): the fitted values at the x_j;
+ *   table_host [cap + 1] (optional, 0 <= cap <= CADDTREE_MAX_CAP): the fit at
+ *       n = 0 .. cap, interpolated linearly between the x_j and continued
+ *       along the end segments outside them, ready to be a plan's
+ *       t_verify_host row (one fit per context length, Sec. 4.6).
+ * Host memory for the solve is allocated internally.  Returns E_INVALID for
+ * bad input and E_UNSUPPORTED if the iteration does not settle. */
+caddtree_status_t caddtree_fit_cost(const double* x_host, const double* y_host, int64_t N, double* fit_host,
+                                    int32_t cap, double* table_host);
+
 const char* caddtree_status_string(caddtree_status_t status);
 const char* caddtree_last_error(void);
 

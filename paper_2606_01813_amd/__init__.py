@@ -29,7 +29,7 @@ import numpy as np
 from . import _lib
 from ._lib import CaddtreeError, MAX_CAP, MAX_CTX, MAX_K, MAX_L
 
-__all__ = ["Plan", "TreeOutputs", "CaddtreeError", "MAX_L", "MAX_K", "MAX_CAP", "MAX_CTX"]
+__all__ = ["Plan", "TreeOutputs", "CaddtreeError", "fit_cost", "MAX_L", "MAX_K", "MAX_CAP", "MAX_CTX"]
 
 
 def _torch():
@@ -46,6 +46,22 @@ def _stream(stream, device) -> int:
     if stream is None:
         stream = torch.cuda.current_stream(device)
     return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def fit_cost(x, y, cap: Optional[int] = None):
+    """Convex non-decreasing least-squares fit of a cost profile (host, ``caddtree_fit_cost``).
+
+    Returns the fitted values at ``x``, and with ``cap`` also the cost table C_v(0 .. cap)."""
+    xs = np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+    ys = np.ascontiguousarray(np.asarray(y, dtype=np.float64))
+    if xs.ndim != 1 or xs.shape != ys.shape:
+        raise ValueError("x and y must be 1-d arrays of equal length")
+    fit = np.empty_like(xs)
+    table = None if cap is None else np.empty(int(cap) + 1, dtype=np.float64)
+    dp = lambda a: None if a is None else a.ctypes.data
+    _lib.check(_lib.lib().caddtree_fit_cost(dp(xs), dp(ys), int(xs.shape[0]), dp(fit),
+                                            -1 if cap is None else int(cap), dp(table)))
+    return fit if cap is None else (fit, table)
 
 
 @dataclasses.dataclass

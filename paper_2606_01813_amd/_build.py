@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libcaddtree.so")
-SOURCES = ["api.cpp", "reduce_topk.hip", "expand.hip", "expand_level.hip", "emit.hip", "accept.hip"]
+SOURCES = ["api.cpp", "reduce_topk.hip", "expand.hip", "expand_level.hip", "emit.hip", "accept.hip", "costfit.cpp"]
 ARCH = os.environ.get("CADDTREE_ARCH", "gfx950")
 
 

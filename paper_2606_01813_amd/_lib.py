@@ -46,7 +46,7 @@ class Outputs(ctypes.Structure):
 
 EXPORTS = [
     "caddtree_plan_create", "caddtree_plan_destroy", "caddtree_workspace_bytes", "caddtree_build",
-    "caddtree_reduce_topk", "caddtree_expand", "caddtree_emit", "caddtree_accept", "caddtree_status_string",
+    "caddtree_reduce_topk", "caddtree_expand", "caddtree_emit", "caddtree_accept", "caddtree_fit_cost", "caddtree_status_string",
     "caddtree_last_error",
 ]
 
@@ -72,6 +72,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.caddtree_emit.restype = ctypes.c_int
     lib.caddtree_accept.argtypes = [vp, vp, vp, vp, i64, vp, vp, i32, vp, vp, vp, vp, vp, vp]
     lib.caddtree_accept.restype = ctypes.c_int
+    lib.caddtree_fit_cost.argtypes = [vp, vp, i64, vp, i32, vp]
+    lib.caddtree_fit_cost.restype = ctypes.c_int
     lib.caddtree_status_string.argtypes = [ctypes.c_int]
     lib.caddtree_status_string.restype = ctypes.c_char_p
     lib.caddtree_last_error.argtypes = []

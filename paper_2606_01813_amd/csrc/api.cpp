@@ -445,4 +445,22 @@ caddtree_status_t caddtree_accept(caddtree_plan_t p, const int32_t* topk_ids, co
   return ok();
 }
 
+caddtree_status_t caddtree_fit_cost(const double* x_host, const double* y_host, int64_t N, double* fit_host,
+                                    int32_t cap, double* table_host) {
+  if (x_host == nullptr || y_host == nullptr) return fail(CADDTREE_E_INVALID, "x_host and y_host are required");
+  if (N < 1) return fail(CADDTREE_E_INVALID, "N = %lld must be >= 1", (long long)N);
+  if (N > ((int64_t)1 << 22)) return fail(CADDTREE_E_UNSUPPORTED, "N = %lld exceeds 2^22", (long long)N);
+  if (table_host != nullptr && (cap < 0 || cap > CADDTREE_MAX_CAP))
+    return fail(CADDTREE_E_INVALID, "cap = %d must be in [0, %d]", cap, CADDTREE_MAX_CAP);
+  for (int64_t j = 0; j < N; ++j) {
+    if (!std::isfinite(x_host[j]) || !std::isfinite(y_host[j]))
+      return fail(CADDTREE_E_INVALID, "profile point %lld is not finite", (long long)j);
+    if (j > 0 && !(x_host[j] > x_host[j - 1]))
+      return fail(CADDTREE_E_INVALID, "x_host is not strictly increasing at %lld", (long long)j);
+  }
+  if (!caddtree::fit_convex_cost(x_host, y_host, (int)N, fit_host, cap, table_host))
+    return fail(CADDTREE_E_UNSUPPORTED, "the active-set iteration did not settle");
+  return ok();
+}
+
 }  // extern "C"

@@ -84,4 +84,9 @@ struct AcceptArgs {
 };
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t stream);
 
+// Host: convex non-decreasing least-squares fit of a cost profile (costfit.cpp); false if the
+// active-set iteration did not settle.
+bool fit_convex_cost(const double* x_host, const double* y_host, int n, double* fit_host, int32_t cap,
+                     double* table_host);
+
 }  // namespace caddtree

@@ -15,12 +15,12 @@ bf16 logits are carried as ``uint16`` bit patterns (round-to-nearest-even from
 fp32); fp32 logits as ``float32``.
 """
 
-from .configs import (CONFIGS, STRESS, VARIANTS, Config, accept_uniforms, cost_table, ctx_lengths, ctx_tables,
-                      get_config)
+from .configs import (CONFIGS, STRESS, VARIANTS, Config, accept_uniforms, cost_profiles, cost_table, ctx_lengths,
+                      ctx_tables, get_config)
 from .gen import draw_round, draw_batch, bf16_bits_from_f32
 
 __all__ = [
     "CONFIGS", "STRESS", "VARIANTS", "Config", "get_config", "cost_table", "ctx_tables", "ctx_lengths",
-    "accept_uniforms",
+    "accept_uniforms", "cost_profiles",
     "draw_round", "draw_batch", "bf16_bits_from_f32",
 ]

@@ -138,6 +138,17 @@ def ctx_lengths(cfg: Config, B: int) -> np.ndarray:
     return ell
 
 
+def cost_profiles(cfg: Config, N: int = 1024, noise: float = 0.01):
+    """Synthetic verification-cost measurements for the offline fit (Sec. 4.6): node counts 1 .. N and, per
+    point of the context grid, the workload's context table at those counts times (1 + noise * z),
+    z ~ N(0, 1).  Returns (n [N] float64, profiles [J, N] float64)."""
+    grid, tables = ctx_tables(cfg.replace(cap=N))
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(cfg.seed, spawn_key=(1 << 28,))))
+    n = np.arange(1, N + 1, dtype=np.float64)
+    prof = tables[:, 1:] * (1.0 + noise * rng.standard_normal((len(grid), N)))
+    return n, prof
+
+
 def accept_uniforms(cfg: Config, B: int, draw: int = 0) -> np.ndarray:
     """Uniforms in [0, 1), float64 [B, L], for drawing target paths in the acceptance simulation; ``draw``
     selects an independent stream (a redraw, or another sample of the same rounds)."""

@@ -517,3 +517,36 @@ def test_accept_mean_is_phi_full_c2():
     se = np.sqrt(a.var(axis=0, ddof=0).mean() / a.size + 1e-12)
     say(f"[accept] c2 mean alpha {a.mean():.4f} mean phi {phi.mean():.4f} se {se:.4f}")
     assert abs(a.mean() - phi.mean()) < 4.5 * max(se, 1e-3)
+
+
+# ------------------------------------------------------------- fitted cost profiles (Sec. 4.6, eq. convex-reg)
+
+def test_plan_from_fitted_profiles():
+    """Noisy cost profiles at 9 context lengths, fitted by the library on the host, drive a context-aware
+    plan; the oracle fits the same profiles and builds the same trees."""
+    from paper_2606_01813_amd import fit_cost
+    cfg = synth.get_config("c1x").replace(V=8000, B=14)
+    grid, _ = synth.ctx_tables(cfg)
+    n, prof = synth.cost_profiles(cfg, N=1024)
+    lib_tables = np.stack([fit_cost(n, prof[j], cap=cfg.cap)[1] for j in range(len(grid))])
+    ora_tables = np.stack([_guard.oracle.costfit.cost_table(n, _guard.oracle.costfit.fit_convex(n, prof[j]),
+                                                              cfg.cap) for j in range(len(grid))])
+    assert np.max(np.abs(lib_tables - ora_tables)) <= 1e-9 * np.max(np.abs(ora_tables))
+    ell = _guard.ctx_inputs(cfg)[2]
+    rounds = list(range(cfg.B))
+    rs, xs = [], []
+    for b in rounds:
+        for a in range(_guard.MAX_ATTEMPTS):
+            x = synth.draw_round(cfg, b, a)
+            tv = _guard.oracle.context_cost(ora_tables, grid, int(ell[b]))
+            r = _guard.oracle.build_round(x, cfg.dtype, cfg.K, cfg.t_draft, tv, cfg.cap, mask=cfg.mask)
+            stop, gap = _guard.oracle.decision_margins(r.exp)
+            if stop >= _guard.TAU and gap >= _guard.TAU:
+                break
+        rs.append(r)
+        xs.append(x)
+    plan = make_plan(cfg, t_verify=lib_tables, ctx_grid=grid)
+    out = run_build(plan, torch_logits(cfg, np.stack(xs)), ctx_len=ctx_tensor(cfg, rounds))
+    h = host(out)
+    say(f"[fit] n*={h['n_star'].tolist()}")
+    compare_tree(h, rs, cfg.mask, cfg.cap)
