@@ -26,6 +26,7 @@ struct caddtree_plan {
   bool use_level;       // the batched expansion applies (see plan_create)
   int device;
   int k1_waves;         // 0 = automatic
+  int k1_unroll;        // 0 = automatic
 };
 
 namespace {
@@ -98,10 +99,6 @@ caddtree_status_t check_logits(const caddtree_plan* p, const void* logits, int64
   return CADDTREE_OK;
 }
 
-int k1_waves(const caddtree_plan* p, int64_t rows) {
-  if (p->k1_waves > 0) return p->k1_waves;
-  return caddtree::reduce_default_waves(rows, (int32_t)p->V, p->dtype);
-}
 
 caddtree_status_t run_reduce(const caddtree_plan* p, const void* logits, int64_t B, int64_t row_stride,
                              int32_t* ids, float* logit, float* lq, double* lse, hipStream_t stream) {
@@ -111,7 +108,9 @@ caddtree_status_t run_reduce(const caddtree_plan* p, const void* logits, int64_t
   a.row_stride = row_stride;
   a.V = (int32_t)p->V;
   a.K = p->K;
-  a.waves_per_row = k1_waves(p, a.rows);
+  const caddtree::ReduceShape sh = caddtree::reduce_default_shape(a.rows, (int32_t)p->V, p->dtype);
+  a.waves_per_row = p->k1_waves > 0 ? p->k1_waves : sh.waves;
+  a.unroll = p->k1_unroll > 0 ? p->k1_unroll : sh.unroll;
   const size_t es = elem_bytes(p->dtype);
   a.aligned = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) && ((size_t)row_stride * es) % 16 == 0;
   a.ids = ids;
@@ -285,6 +284,11 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
   if (const char* env = std::getenv("CADDTREE_K1_WAVES")) {
     const int w = std::atoi(env);
     if (w == 1 || w == 2 || w == 4 || w == 8 || w == 16) p->k1_waves = w;
+  }
+  p->k1_unroll = 0;
+  if (const char* env = std::getenv("CADDTREE_K1_UNROLL")) {
+    const int u = std::atoi(env);
+    if (u == 4 || u == 8) p->k1_unroll = u;
   }
   hipError_t e = hipGetDevice(&p->device);
   if (e != hipSuccess) { delete p; return hip_fail(e, "hipGetDevice"); }

@@ -18,6 +18,7 @@ struct ReduceArgs {
   int32_t V;
   int32_t K;
   int32_t waves_per_row; // 1 .. 16
+  int32_t unroll;        // 16-byte loads in flight per lane: 4 or 8
   bool aligned;          // rows start on 16-byte boundaries
   int32_t* ids;          // [rows, K]
   float* logit;          // [rows, K]
@@ -25,7 +26,11 @@ struct ReduceArgs {
   double* lse;           // [rows]
 };
 hipError_t launch_reduce_topk(const ReduceArgs& a, caddtree_dtype_t dtype, hipStream_t stream);
-int reduce_default_waves(int64_t rows, int32_t V, caddtree_dtype_t dtype);
+struct ReduceShape {
+  int32_t waves;   // waves per row
+  int32_t unroll;  // 16-byte loads in flight per lane
+};
+ReduceShape reduce_default_shape(int64_t rows, int32_t V, caddtree_dtype_t dtype);
 
 // Stage 2: best-first expansion with the greedy stop, one workgroup per round.
 struct ExpandArgs {

@@ -32,10 +32,6 @@ namespace caddtree {
 namespace {
 
 constexpr int kWave = 64;
-#ifndef CADDTREE_K1_UNROLL
-#define CADDTREE_K1_UNROLL 4
-#endif
-constexpr int kUnroll = CADDTREE_K1_UNROLL;   // 16-byte loads in flight per lane
 constexpr float kLog2eHi = 0x1.715476p+0f;     // log2(e) rounded to fp32
 constexpr float kLog2eLo = 0x1.4ae0c0p-26f;    // log2(e) - kLog2eHi, rounded to fp32
 constexpr double kLog2eD = 0x1.71547652b82fep+0;
@@ -180,7 +176,8 @@ __device__ __forceinline__ unsigned load_guarded(const T* rowp, int e, int V, fl
   return ok;
 }
 
-template <typename T, bool kAligned>
+// kUnroll: 16-byte loads in flight per lane (4 or 8)
+template <typename T, bool kAligned, int kUnroll>
 __global__ void __launch_bounds__(1024)
 reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int K,
                    int32_t* __restrict__ out_ids, float* __restrict__ out_logit,
@@ -304,20 +301,39 @@ template <typename T, bool A>
 hipError_t launch_t(const ReduceArgs& a, hipStream_t stream) {
   const dim3 grid((unsigned)a.rows);
   const dim3 block((unsigned)(kWave * a.waves_per_row));
-  hipLaunchKernelGGL((reduce_topk_kernel<T, A>), grid, block, 0, stream,
-                     static_cast<const T*>(a.logits), a.row_stride, a.V, a.K,
-                     a.ids, a.logit, a.lq, a.lse);
+  if (a.unroll == 8)
+    hipLaunchKernelGGL((reduce_topk_kernel<T, A, 8>), grid, block, 0, stream,
+                       static_cast<const T*>(a.logits), a.row_stride, a.V, a.K,
+                       a.ids, a.logit, a.lq, a.lse);
+  else
+    hipLaunchKernelGGL((reduce_topk_kernel<T, A, 4>), grid, block, 0, stream,
+                       static_cast<const T*>(a.logits), a.row_stride, a.V, a.K,
+                       a.ids, a.logit, a.lq, a.lse);
   return hipGetLastError();
 }
 
 }  // namespace
 
-int reduce_default_waves(int64_t rows, int32_t V, caddtree_dtype_t dtype) {
+// Launch shape.  The stream keeps HBM busy when about 32 MiB of loads are in
+// flight across the chip (resident waves x loads per lane x 1 KiB), and a row
+// split over fewer waves pays less for the start of each segment and for the
+// final merge.  Large batches: one wave per row, 8 loads in flight for bf16
+// (its kernel then holds 4 waves per SIMD, 4096 on the chip) and 4 for fp32
+// (8 per SIMD).  Batches of at most 4096 rows: 8 loads in flight, and the
+// fewest waves per row that still put 4096 waves on the chip at once.
+ReduceShape reduce_default_shape(int64_t rows, int32_t V, caddtree_dtype_t dtype) {
   const int CH = kWave * (dtype == CADDTREE_BF16 ? 8 : 4);
   const int nch = (V + CH - 1) / CH;
-  int s = 1;
-  while (s < 16 && rows * s < 16384 && nch / (2 * s) >= 4) s *= 2;
-  return s;
+  ReduceShape sh{1, 4};
+  if (rows >= 8192) {
+    sh.unroll = dtype == CADDTREE_BF16 ? 8 : 4;
+  } else if (rows > 4096) {
+    sh.unroll = 4;
+  } else {
+    sh.unroll = 8;
+    while (sh.waves < 16 && rows * sh.waves * 2 <= 4096 && nch / (2 * sh.waves) >= 16) sh.waves *= 2;
+  }
+  return sh;
 }
 
 hipError_t launch_reduce_topk(const ReduceArgs& a, caddtree_dtype_t dtype, hipStream_t stream) {

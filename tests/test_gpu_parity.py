@@ -550,3 +550,16 @@ def test_plan_from_fitted_profiles():
     h = host(out)
     say(f"[fit] n*={h['n_star'].tolist()}")
     compare_tree(h, rs, cfg.mask, cfg.cap)
+
+
+@pytest.mark.parametrize("waves", [1, 2, 4, 8, 16])
+@pytest.mark.parametrize("unroll", [4, 8])
+def test_k1_launch_shapes(waves, unroll, monkeypatch):
+    """Every split of a row over 1 .. 16 wavefronts and both load depths give the oracle's top-K table
+    and trees (the shape only changes the order of the fp64 partial sums)."""
+    monkeypatch.setenv("CADDTREE_K1_WAVES", str(waves))
+    monkeypatch.setenv("CADDTREE_K1_UNROLL", str(unroll))
+    cfg = synth.get_config("c1").replace(V=70001, B=3)
+    _parity_batch(cfg, list(range(cfg.B)))
+    cfg32 = synth.get_config("c4").replace(V=30011, B=2, L=8)
+    _parity_batch(cfg32, list(range(cfg32.B)))
