@@ -1,6 +1,7 @@
 // Host side of the C ABI declared in caddtree.h: plan creation and validation,
 // workspace sizing, argument checks and launch sequencing on the caller's stream.
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -235,7 +236,8 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
     }
   }
   const int cap = cfg->budget_cap;
-  double min_c1 = INFINITY;
+  int flat_start = 0;     // the most leading zero marginal costs over the tables
+  bool convex = true;
   for (int j = 0; j < J; ++j) {
     const double* tv = cfg->t_verify_host + (size_t)j * (size_t)(cap + 1);
     double scale = 0.0;
@@ -248,12 +250,16 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
     for (int n = 1; n <= cap; ++n)
       if (tv[n] - tv[n - 1] < -slack)
         return fail(CADDTREE_E_COST, "C_v of table %d decreases between n = %d and %d", j, n - 1, n);
-    if (!(cfg->flags & CADDTREE_ALLOW_NONCONVEX))
-      for (int n = 2; n <= cap; ++n)
-        if ((tv[n] - tv[n - 1]) - (tv[n - 1] - tv[n - 2]) < -slack)
+    for (int n = 2; n <= cap; ++n)
+      if ((tv[n] - tv[n - 1]) - (tv[n - 1] - tv[n - 2]) < -slack) {
+        if (!(cfg->flags & CADDTREE_ALLOW_NONCONVEX))
           return fail(CADDTREE_E_COST, "C_v of table %d is not convex at n = %d (Assumption 1 needs convex cost)",
                       j, n - 1);
-    if (cap >= 1) min_c1 = std::fmin(min_c1, tv[1] - tv[0]);
+        convex = false;
+      }
+    int m0 = 0;
+    while (m0 < cap && !(tv[m0 + 1] > tv[m0])) ++m0;
+    flat_start = std::max(flat_start, m0);
   }
 
   caddtree_plan* p = new (std::nothrow) caddtree_plan();
@@ -269,14 +275,16 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
   p->n_ctx = J;
   p->d_t_verify = nullptr;
   p->d_ctx_grid = nullptr;
-  // The batched expansion needs a threshold search that settles within its LDS
-  // store: costs that rise from the first node on (C_v(1) > C_v(0) in every
-  // table), or a fixed budget of at most 128 nodes.  Flat-start costs keep
-  // theta rising for many nodes, and go to the serial kernel.
+  // The batched expansion finds the stop by bisection, which needs theta to be
+  // unimodal along the pop order (a convex cost, Thm. 1), and a threshold set
+  // that holds the tree within its capacity (512 nodes): a fixed budget of at
+  // most 256 nodes, or a cost whose marginal turns positive within the first
+  // 256 nodes in every table (the tree holds at least that many nodes).
+  const int level_cap = caddtree::expand_level_capacity();
   if (cfg->flags & CADDTREE_FIXED_BUDGET)
-    p->use_level = cap >= 1 && cap <= 128;
+    p->use_level = cap >= 1 && cap <= level_cap / 2;
   else
-    p->use_level = cap >= 1 && min_c1 > 0.0;
+    p->use_level = cap >= 1 && convex && flat_start < level_cap / 2;
   if (const char* env = std::getenv("CADDTREE_EXPAND")) {
     if (std::strcmp(env, "serial") == 0) p->use_level = false;
   }

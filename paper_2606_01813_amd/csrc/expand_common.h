@@ -29,6 +29,40 @@ __device__ __forceinline__ uint32_t rl_u(uint32_t v, int l) { return (uint32_t)_
 
 __host__ __device__ __forceinline__ size_t a16(size_t x) { return (x + 15) & ~(size_t)15; }
 
+// ---- wave scans through DPP (gfx9: row_shr within 16-lane rows, then row_bcast:15 / :31 across rows)
+template <int CTRL, int ROW_MASK, bool BOUND>
+__device__ __forceinline__ int dpp_i(int old, int v) {
+  return __builtin_amdgcn_update_dpp(old, v, CTRL, ROW_MASK, 0xF, BOUND);
+}
+template <int CTRL, int ROW_MASK, bool BOUND>
+__device__ __forceinline__ double dpp_d(double v) {
+  const uint64_t u = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = (uint32_t)dpp_i<CTRL, ROW_MASK, BOUND>(0, (int)(uint32_t)u);
+  const uint32_t hi = (uint32_t)dpp_i<CTRL, ROW_MASK, BOUND>(0, (int)(uint32_t)(u >> 32));
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+// inclusive prefix sum over the 64 lanes (lane order)
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  x += dpp_i<0x111, 0xF, true>(0, x);
+  x += dpp_i<0x112, 0xF, true>(0, x);
+  x += dpp_i<0x114, 0xF, true>(0, x);
+  x += dpp_i<0x118, 0xF, true>(0, x);
+  x += dpp_i<0x142, 0xA, false>(0, x);
+  x += dpp_i<0x143, 0xC, false>(0, x);
+  return x;
+}
+__device__ __forceinline__ double wave_incl_scan(double x) {
+  x += dpp_d<0x111, 0xF, true>(x);
+  x += dpp_d<0x112, 0xF, true>(x);
+  x += dpp_d<0x114, 0xF, true>(x);
+  x += dpp_d<0x118, 0xF, true>(x);
+  x += dpp_d<0x142, 0xA, false>(x);
+  x += dpp_d<0x143, 0xC, false>(x);
+  return x;
+}
+// the value of lane - 1 (0 in lane 0)
+__device__ __forceinline__ double wave_shr1(double x) { return dpp_d<0x138, 0xF, true>(x); }
+
 // Round cost C(n) = C_d + C_v(n; l) (Sec. 4.2).  With a context-length grid
 // L_0 < .. < L_{J-1} and one table C_v(.; L_j) per grid point (Sec. 4.6), a
 // round at context length l with L_j <= l < L_{j+1} uses the linear

@@ -8,28 +8,37 @@
 //
 //  1. build T(tau) level by level from the root.  The children of a node that
 //     reach the threshold are a prefix of its ranks (sigma falls with the rank),
-//     so each lane counts its node's children, an exclusive scan gives their
-//     slots, and the set comes out in breadth-first order (depth, then rank
-//     tuple), which is also the tie-break of the pop order within a depth;
-//  2. rank the set by the pop order (each lane counts the nodes before its own;
-//     exact sigma ties fall back to depth, Lambda and generation order);
-//  3. run the stop rule: Phi accumulates in pop order exactly as the sequential
-//     loop does (one lane), theta for every position follows in parallel, and
-//     the first position whose theta does not rise (or the cap) ends the tree;
-//  4. if every node of T(tau) was kept and the tree continues below tau, lower
-//     tau and start again; if T(tau) outgrows its LDS capacity, raise tau
+//     so each lane counts its node's children, a prefix sum gives their slots,
+//     and the set comes out in breadth-first order (depth, then rank tuple),
+//     which is also the tie-break of the pop order within a depth;
+//  2. find where the greedy stop falls along the pop order of T(tau):
+//     * up to 64 nodes: each lane ranks its node by counting the nodes that
+//       pop before it (the full order with its tie-breaks, one pass), the
+//       path probabilities are scattered into pop order, a prefix sum gives
+//       Phi before every position m, and m is kept iff
+//       (1 + Phi_m + delta_m) / C(m + 1) > (1 + Phi_m) / C(m) and m < cap;
+//     * larger sets: under a convex cost theta rises and then falls along the
+//       pop order (Thm. 1), so "position m is kept" holds below n* and fails
+//       from n* on, and a bisection over pivot nodes finds n*: a pivot's
+//       position and the Phi before it are a count and a sum over the nodes
+//       that pop before it;
+//     with a fixed budget m is kept iff m < cap;
+//  3. if every node of T(tau) is kept and the tree continues below tau, lower
+//     tau and start again; if T(tau) outgrows its capacity, raise tau
 //     (bisection between the two).
 //
-// The initial tau comes from the cost model: a node kept at a position near n
-// has delta > (1 + Phi) c_{n+1} / C(n) (Lemma 1), so the stop lies around
-// log(2 c_1 / C(32)).  A round that does not settle within kMaxAttempts, or
-// whose tree needs more than kSCap nodes, is flagged (n_star = -1) and left to
-// the serial kernel, which gives the same result.  Costs with a flat start
-// (c_1 = 0) go straight to the serial kernel: the threshold search converges
-// slowly there.
+// The initial tau comes from the cost model: a node kept near position n has
+// delta > (1 + Phi) c_{n+1} / C(n) (Lemma 1); with c_{m0+1} the first positive
+// marginal cost the stop lies past m0, around delta = (1 + Phi) c / C with Phi
+// of order one.  A round that does not settle within kMaxAttempts, or whose
+// tree needs more than kSCap nodes, is flagged (n_star = -1) and left to the
+// serial kernel, which gives the same tree.
 //
 // The kept nodes are a prefix of the pop order and a prefix-closed set, so
 // their breadth-first positions are a running count over generation order.
+// Phi here is a prefix sum over the wave rather than a left-to-right sum in
+// pop order: it matches the sequential sum to rounding, and the tree does not
+// depend on it except at stop margins of that size.
 
 #include <cmath>
 
@@ -42,65 +51,184 @@ namespace {
 using namespace xp;
 
 constexpr int kW = 64;
-constexpr int kSCap = 256;        // nodes of T(tau) held at once
-constexpr int kMaxAttempts = 14;
+constexpr int kSCap = 512;            // nodes of T(tau) held at once
+constexpr int kCW = 66;               // C(0 .. 65) cached in LDS
+constexpr int kMaxAttempts = 12;
 
-__device__ __forceinline__ int excl_scan(int v, int lane, int* total) {
-  int x = v;
-#pragma unroll
-  for (int o = 1; o < kW; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  *total = __shfl(x, kW - 1);
-  return x - v;
+// One node of T(tau): sigma, Lambda, and its packed word (parent, rank, depth)
+// with the generation index in the top 9 bits.
+struct Node {
+  double s;
+  double l;
+  uint32_t m;
+};
+
+__device__ __forceinline__ int n_gen(uint32_t m) { return (int)(m >> 23); }
+
+// node a pops before node b (sigma desc, depth asc, Lambda desc, generation index asc;
+// within a depth the generation order is the rank-tuple order)
+__device__ __forceinline__ bool pops_before(double sa, double la, uint32_t ma, double sb, double lb, uint32_t mb) {
+  const int da = m_depth(ma), db = m_depth(mb);
+  return sa > sb || (sa == sb && (da < db || (da == db && (la > lb || (la == lb && n_gen(ma) < n_gen(mb))))));
+}
+__device__ __forceinline__ bool pops_before(const Node& a, const Node& b) {
+  return pops_before(a.s, a.l, a.m, b.s, b.l, b.m);
 }
 
 struct Lds {
   float* tl;        // [L * K] raw logits
   int32_t* tid;     // [L * K] token ids
-  double* cw;       // [W] C(0 .. W - 1) = C_d + C_v
-  double* sig;      // T(tau), generation order
-  double* lam;
-  uint32_t* meta;
-  int16_t* rnk;     // pop-order rank of each node of T(tau)
-  int16_t* pos;     // breadth-first position of each kept node
-  double* dsort;    // delta in pop order
-  double* P;        // Phi before each position
-  double* th;       // theta_new at each position
+  double* cw;       // [kCW] C(0 .. kCW - 1) = C_d + C_v
+  double2* sl;      // T(tau) in generation order: (sigma, Lambda)
+  uint32_t* meta;   //   packed word with the generation index
+  double* dsort;    // path probabilities in pop order (small sets)
+  int16_t* pos;     // kept flag, then breadth-first position, of each node
 };
 
-__host__ __device__ __forceinline__ size_t level_lds_bytes(size_t LK, size_t W) {
+__host__ __device__ __forceinline__ size_t level_lds_bytes(size_t LK) {
   size_t off = 0;
   off = a16(off + 4 * LK);
   off = a16(off + 4 * LK);
-  off = a16(off + 8 * W);
-  off = a16(off + 8 * kSCap);
-  off = a16(off + 8 * kSCap);
+  off = a16(off + 8 * kCW);
+  off = a16(off + 16 * kSCap);
   off = a16(off + 4 * kSCap);
+  off = a16(off + 8 * kW);
   off = a16(off + 2 * kSCap);
-  off = a16(off + 2 * kSCap);
-  off = a16(off + 8 * kSCap);
-  off = a16(off + 8 * (kSCap + 1));
-  off = a16(off + 8 * kSCap);
   return off;
 }
 
-__device__ Lds carve(unsigned char* smem, size_t LK, size_t W) {
+__device__ Lds carve(unsigned char* smem, size_t LK) {
   Lds s;
   size_t off = 0;
   s.tl = reinterpret_cast<float*>(smem + off);      off = a16(off + 4 * LK);
   s.tid = reinterpret_cast<int32_t*>(smem + off);   off = a16(off + 4 * LK);
-  s.cw = reinterpret_cast<double*>(smem + off);     off = a16(off + 8 * W);
-  s.sig = reinterpret_cast<double*>(smem + off);    off = a16(off + 8 * kSCap);
-  s.lam = reinterpret_cast<double*>(smem + off);    off = a16(off + 8 * kSCap);
+  s.cw = reinterpret_cast<double*>(smem + off);     off = a16(off + 8 * kCW);
+  s.sl = reinterpret_cast<double2*>(smem + off);    off = a16(off + 16 * kSCap);
   s.meta = reinterpret_cast<uint32_t*>(smem + off); off = a16(off + 4 * kSCap);
-  s.rnk = reinterpret_cast<int16_t*>(smem + off);   off = a16(off + 2 * kSCap);
-  s.pos = reinterpret_cast<int16_t*>(smem + off);   off = a16(off + 2 * kSCap);
-  s.dsort = reinterpret_cast<double*>(smem + off);  off = a16(off + 8 * kSCap);
-  s.P = reinterpret_cast<double*>(smem + off);      off = a16(off + 8 * (kSCap + 1));
-  s.th = reinterpret_cast<double*>(smem + off);
+  s.dsort = reinterpret_cast<double*>(smem + off);  off = a16(off + 8 * kW);
+  s.pos = reinterpret_cast<int16_t*>(smem + off);
   return s;
+}
+
+struct Cost {
+  const double* cw;
+  RoundCost C;
+  __device__ __forceinline__ double operator()(int n) const { return n < kCW ? cw[n] : C(n); }
+};
+
+struct Stop {
+  int n;        // first position not kept, or ns when every position is kept
+  double phi;   // Phi before position n
+};
+
+// up to 64 nodes: rank by counting, Phi by a prefix sum over pop positions;
+// on a stop inside the set, the kept flags go to s.pos by generation index
+__device__ Stop stop_small(const Lds& s, int ns, int cap, int fixed, const Cost& cost, int lane) {
+  const bool live = lane < ns;
+  const int i = live ? lane : 0;
+  const double2 me = s.sl[i];
+  const uint32_t mm = s.meta[i];
+  int r = 0;
+#pragma unroll 4
+  for (int j = 0; j < ns; ++j) {
+    const double2 o = s.sl[j];
+    const uint32_t om = s.meta[j];
+    r += pops_before(o.x, o.y, om, me.x, me.y, mm) ? 1 : 0;
+  }
+  if (live) s.dsort[r] = exp(me.x);
+  __syncthreads();
+  const double d = lane < ns ? s.dsort[lane] : 0.0;
+  const double incl = wave_incl_scan(d);
+  const double pe = wave_shr1(incl);          // Phi before position `lane`
+  bool keep = lane < cap;
+  if (keep && !fixed && lane < ns) keep = (1.0 + pe + d) / cost(lane + 1) > (1.0 + pe) / cost(lane);
+  const unsigned long long fm = __ballot(lane < ns && !keep);
+  if (!fm) return Stop{ns, rl_d(incl, kW - 1)};
+  const int stop = __builtin_ctzll(fm);
+  if (live) s.pos[lane] = r < stop ? 1 : 0;
+  return Stop{stop, rl_d(pe, stop)};
+}
+
+// larger sets: bisection over pivots (P nodes per lane, position e = j * 64 + lane
+// in generation order)
+template <int P>
+__device__ Stop stop_large(const Lds& s, int ns, int cap, int fixed, const Cost& cost, int lane, unsigned seed) {
+  Node x[P];
+  double dl[P];
+#pragma unroll
+  for (int j = 0; j < P; ++j) {
+    const int e = j * kW + lane;
+    if (e < ns) {
+      const double2 v = s.sl[e];
+      x[j] = Node{v.x, v.y, s.meta[e]};
+      dl[j] = exp(v.x);
+    } else {
+      x[j] = Node{-INFINITY, 0.0, (63u << 17) | ((uint32_t)e << 23)};
+      dl[j] = 0.0;
+    }
+  }
+  bool hasA = false, hasB = false;
+  Node A{0.0, 0.0, 0u}, B{0.0, 0.0, 0u};
+  int posB = 0;
+  double phiB = 0.0;
+  unsigned rng = seed;
+  for (;;) {
+    unsigned long long cm[P];
+    int total = 0;
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      bool c = j * kW + lane < ns;
+      if (hasA) c = c && pops_before(A, x[j]);
+      if (hasB) c = c && pops_before(x[j], B);
+      cm[j] = __ballot(c);
+      total += __popcll(cm[j]);
+    }
+    if (total == 0) break;
+    rng = rng * 1664525u + 1013904223u;
+    int k = (int)((rng >> 8) % (unsigned)total);
+    int pj = 0;
+    unsigned long long mk = cm[0];
+#pragma unroll
+    for (int j = 0; j + 1 < P; ++j) {
+      const int c = __popcll(cm[j]);
+      if (pj == j && k >= c) { k -= c; pj = j + 1; mk = cm[j + 1]; }
+    }
+    const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(mk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mk, 0));
+    const int pl = __builtin_ctzll(__ballot(((mk >> lane) & 1ull) && below == k));
+    Node pv{0.0, 0.0, 0u};
+    double pd = 0.0;
+#pragma unroll
+    for (int j = 0; j < P; ++j)
+      if (j == pj) {
+        pv = Node{rl_d(x[j].s, pl), rl_d(x[j].l, pl), rl_u(x[j].m, pl)};
+        pd = rl_d(dl[j], pl);
+      }
+    int cnt = 0;
+    double part = 0.0;
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      const bool bf = j * kW + lane < ns && pops_before(x[j], pv);
+      cnt += __popcll(__ballot(bf));
+      part += bf ? dl[j] : 0.0;
+    }
+    const double ph = rl_d(wave_incl_scan(part), kW - 1);
+    bool keep = cnt < cap;
+    if (keep && !fixed) keep = (1.0 + ph + pd) / cost(cnt + 1) > (1.0 + ph) / cost(cnt);
+    if (keep) { hasA = true; A = pv; }
+    else { hasB = true; B = pv; posB = cnt; phiB = ph; }
+  }
+  if (!hasB) {
+    double part = 0.0;
+#pragma unroll
+    for (int j = 0; j < P; ++j) part += dl[j];
+    return Stop{ns, rl_d(wave_incl_scan(part), kW - 1)};
+  }
+#pragma unroll
+  for (int j = 0; j < P; ++j) {
+    const int e = j * kW + lane;
+    if (e < ns) s.pos[e] = pops_before(x[j], B) ? 1 : 0;
+  }
+  return Stop{posB, phiB};
 }
 
 __global__ void __launch_bounds__(kW)
@@ -114,15 +242,14 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   const int b = blockIdx.x;
   const int lane = threadIdx.x;
   const int LK = L * K;
-  const int W = (cap < kSCap ? cap : kSCap) + 2;
-  const Lds s = carve(smem, (size_t)LK, (size_t)W);
-  const RoundCost C = ct.round(b);
+  const Lds s = carve(smem, (size_t)LK);
+  const Cost cost{s.cw, ct.round(b)};
 
   for (int i = lane; i < LK; i += kW) {
     s.tl[i] = topk_logit[(int64_t)b * LK + i];
     s.tid[i] = topk_ids[(int64_t)b * LK + i];
   }
-  for (int i = lane; i < W; i += kW) s.cw[i] = i <= cap ? C(i) : 1.0;
+  for (int i = lane; i < kCW; i += kW) s.cw[i] = i <= cap ? cost.C(i) : 1.0;
   // lane d holds A_d = sum_{i<=d} LSE_i, summed in depth order (d = 0 .. L)
   const double lse_l = lane < L ? lse[(int64_t)b * L + lane] : 0.0;
   double Areg = 0.0;
@@ -139,15 +266,32 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   const double A1 = rl_d(Areg, 1);
   const double top = pmin(0.0 + (double)s.tl[0] - A1, 0.0);   // the first node to pop
   double tau = top - 3.0;
-  if (!fixed && s.cw[1] - s.cw[0] > 0.0) {
-    const int m = cap < 32 ? cap : 32;
-    tau = log(2.0 * (s.cw[1] - s.cw[0]) / s.cw[m]) - 0.5;
+  int need = 1;                              // the tree holds at least this many nodes
+  if (!fixed && cap >= 1) {
+    // the first positive marginal cost c_{m0 + 1} (the stop lies past m0)
+    int m0 = -1;
+    for (int i0 = 0; i0 < kSCap && i0 < cap && m0 < 0; i0 += kW) {
+      const int i = i0 + lane;
+      const bool up = i < cap && i < kSCap && cost(i + 1) > cost(i);
+      const unsigned long long m = __ballot(up);
+      if (m) m0 = i0 + __builtin_ctzll(m);
+    }
+    if (m0 < 0 || m0 >= kSCap / 2) {         // flat for too long: the serial kernel's case
+      if (lane == 0) n_star_out[b] = -1;
+      return;
+    }
+    need = m0 + 1;
+    const int m = m0 + 32 < cap ? m0 + 32 : cap;
+    tau = log(2.0 * (cost(m0 + 1) - cost(m0)) / cost(m)) - 0.5;
+  } else if (fixed) {
+    need = cap;
   }
   tau = fmin(tau, top);
 
   double lo = -INFINITY, hi = INFINITY;
   int n = 0, ns = 0;
   double phi = 0.0, theta = theta0;
+  bool all_kept = false;                    // every node of T(tau) is kept (no flags written)
   bool done = cap == 0;
   for (int attempt = 0; attempt < kMaxAttempts && !done; ++attempt) {
     // ---- 1. T(tau), level by level
@@ -157,34 +301,36 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       double x = 0.0, l1 = 0.0;
       if (live) { l1 = 0.0 + (double)s.tl[lane]; x = l1 - A1; }
       const bool in = live && x >= tau;     // the ranks that qualify form a prefix
-      if (in) { s.sig[lane] = pmin(x, 0.0); s.lam[lane] = l1; s.meta[lane] = pack(-1, lane, 1); }
+      if (in) { s.sl[lane] = make_double2(pmin(x, 0.0), l1); s.meta[lane] = pack(-1, lane, 1) | ((uint32_t)lane << 23); }
       ns = __popcll(__ballot(in));
       cut = ns < K;
     }
     int la = 0, lb = ns;                    // the current level is [la, lb)
     for (int d = 1; d < L && la < lb && !over; ++d) {
       __syncthreads();
-      const double Ad = __shfl(Areg, d + 1);
+      const double Ad = rl_d(Areg, d + 1);
       int nb = lb;
       for (int p0 = la; p0 < lb; p0 += kW) {
         const int p = p0 + lane;
         const bool live = p < lb;
-        const int pp = live ? p : la;
-        const double ps = s.sig[pp], pl = s.lam[pp];
+        const double2 pv = s.sl[live ? p : la];
         int c = 0;
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          c += (live && r < K && (pl + (double)s.tl[d * K + (r < K ? r : 0)]) - Ad >= tau) ? 1 : 0;
-        int tot = 0;
-        const int off = excl_scan(c, lane, &tot);
+          c += (live && r < K && (pv.y + (double)s.tl[d * K + (r < K ? r : 0)]) - Ad >= tau) ? 1 : 0;
+        const int incl = wave_incl_scan(c);
+        const int tot = __builtin_amdgcn_readlane(incl, kW - 1);
+        const int off = incl - c;
         if (live && c < K) cut = true;
         if (nb + tot > kSCap) { over = true; break; }
-        for (int r = 0; r < c; ++r) {
-          const int i = nb + off + r;
-          const double l = pl + (double)s.tl[d * K + r];
-          s.sig[i] = pmin(l - Ad, ps);
-          s.lam[i] = l;
-          s.meta[i] = pack(p, r, d + 1);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          if (r < c) {
+            const int i = nb + off + r;
+            const double l = pv.y + (double)s.tl[d * K + r];
+            s.sl[i] = make_double2(pmin(l - Ad, pv.x), l);
+            s.meta[i] = pack(p, r, d + 1) | ((uint32_t)i << 23);
+          }
         }
         nb += tot;
       }
@@ -200,71 +346,36 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       continue;
     }
     ns = lb;
-    __syncthreads();
-
-    // ---- 2. pop-order rank
-    for (int i0 = 0; i0 < ns; i0 += kW) {
-      const int i = i0 + lane;
-      const bool live = i < ns;
-      const double si = live ? s.sig[i] : INFINITY;
-      int r = 0, ties = 0;
-#pragma unroll 8
-      for (int j = 0; j < ns; ++j) {
-        const double sj = s.sig[j];
-        r += sj > si ? 1 : 0;
-        ties += sj == si ? 1 : 0;
-      }
-      if (__ballot(live && ties > 1)) {
-        const int di = live ? m_depth(s.meta[i]) : 0;
-        const double li = live ? s.lam[i] : 0.0;
-        int rt = 0;
-#pragma unroll 8
-        for (int j = 0; j < ns; ++j) {
-          const double sj = s.sig[j], lj = s.lam[j];
-          const int dj = m_depth(s.meta[j]);
-          rt += (sj == si && j != i && (dj < di || (dj == di && (lj > li || (lj == li && j < i))))) ? 1 : 0;
-        }
-        r += (live && ties > 1) ? rt : 0;
-      }
-      if (live) {
-        s.rnk[i] = (int16_t)r;
-        s.dsort[r] = exp(si);
-      }
+    if (cut && ns < need && ns < cap) {     // too few nodes to hold the stop: lower tau without selecting
+      hi = tau;
+      tau = lo > -INFINITY ? 0.5 * (tau + lo) : tau - 1.5;
+      continue;
     }
     __syncthreads();
 
-    // ---- 3. stop rule
-    if (lane == 0) {
-      double acc = 0.0;
-      for (int k = 0; k < ns; ++k) { s.P[k] = acc; acc = acc + s.dsort[k]; }
-      s.P[ns] = acc;
-    }
-    __syncthreads();
-    for (int k = lane; k < ns; k += kW) {
-      if (k < cap) {
-        const int m = k + 1;
-        const double c = m < W ? s.cw[m] : C(m);
-        s.th[k] = (1.0 + s.P[k] + s.dsort[k]) / c;
-      }
-    }
-    __syncthreads();
-    int kk = ns;
-    for (int k0 = 0; k0 < ns; k0 += kW) {
-      const int k = k0 + lane;
-      bool stop = false;
-      if (k < ns) stop = k >= cap || (!fixed && s.th[k] <= (k == 0 ? theta0 : s.th[k - 1]));
-      const unsigned long long ms = __ballot(stop);
-      if (ms) { kk = k0 + __builtin_ctzll(ms); break; }
-    }
-    if (kk < ns || kk >= cap || !cut) {     // stopped inside, hit the cap, or the whole tree is here
-      n = kk;
-      phi = s.P[kk];
-      theta = kk == 0 ? theta0 : s.th[kk - 1];
+    // ---- 2. where the stop falls
+    Stop st;
+    const unsigned seed = 0x9E3779B9u ^ (unsigned)b ^ ((unsigned)attempt << 16);
+    if (ns <= kW) st = stop_small(s, ns, cap, fixed, cost, lane);
+    else if (ns <= 2 * kW) st = stop_large<2>(s, ns, cap, fixed, cost, lane, seed);
+    else if (ns <= 4 * kW) st = stop_large<4>(s, ns, cap, fixed, cost, lane, seed);
+    else st = stop_large<8>(s, ns, cap, fixed, cost, lane, seed);
+
+    if (st.n < ns) {                        // the stop (or the cap) falls inside T(tau)
+      n = st.n;
+      phi = st.phi;
+      all_kept = false;
+      done = true;
+    } else if (!cut || ns >= cap) {         // the whole tree (or the cap) is here and all of it is kept
+      n = ns;
+      phi = st.phi;
+      all_kept = true;
       done = true;
     } else {                                // every node kept: the stop lies below tau
       hi = tau;
       tau = lo > -INFINITY ? 0.5 * (tau + lo) : tau - 1.5;
     }
+    if (done) theta = n == 0 ? theta0 : (1.0 + phi) / cost(n);
   }
   if (!done) {
     if (lane == 0) n_star_out[b] = -1;      // left to the serial kernel
@@ -278,26 +389,27 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   if (n == 0) return;
 
   // ---- breadth-first positions: kept nodes before this one in generation order
+  __syncthreads();                          // the kept flags written by the selection
   int base = 0;
   for (int i0 = 0; i0 < ns; i0 += kW) {
     const int i = i0 + lane;
-    const bool kept = i < ns && s.rnk[i] < n;
+    const bool kept = i < ns && (all_kept || s.pos[i] != 0);
     const unsigned long long m = __ballot(kept);
     const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
-    if (kept) s.pos[i] = (int16_t)(base + below);
+    if (i < ns) s.pos[i] = kept ? (int16_t)(base + below) : (int16_t)-1;
     base += __popcll(m);
   }
   __syncthreads();
   const int64_t ob = (int64_t)b * cap;
   for (int i = lane; i < ns; i += kW) {
-    if (s.rnk[i] < n) {
+    const int o = s.pos[i];
+    if (o >= 0) {
       const uint32_t m = s.meta[i];
       const int p = m_parent(m), d = m_depth(m), r = m_rank(m);
-      const int o = s.pos[i];
       token_ids[ob + o] = s.tid[(d - 1) * K + r];
       parent_out[ob + o] = p < 0 ? -1 : (int)s.pos[p];
       depth_out[ob + o] = d;
-      if (path_prob) path_prob[ob + o] = (float)exp(s.sig[i]);
+      if (path_prob) path_prob[ob + o] = (float)exp(s.sl[i].x);
     }
   }
 }
@@ -305,9 +417,11 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
 }  // namespace
 
 size_t expand_level_lds_bytes(int32_t L, int32_t K, int32_t cap) {
-  const size_t W = (cap < kSCap ? (size_t)cap : kSCap) + 2;
-  return level_lds_bytes((size_t)L * K, W);
+  (void)cap;
+  return level_lds_bytes((size_t)L * K);
 }
+
+int expand_level_capacity() { return kSCap; }
 
 hipError_t launch_expand_level(const ExpandArgs& a, hipStream_t stream) {
   if (a.B == 0) return hipSuccess;

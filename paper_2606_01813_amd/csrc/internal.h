@@ -55,6 +55,7 @@ hipError_t expand_prepare(int32_t L, int32_t K, int32_t cap);  // raises the dyn
 hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream);
 hipError_t launch_expand_level(const ExpandArgs& a, hipStream_t stream);
 size_t expand_level_lds_bytes(int32_t L, int32_t K, int32_t cap);
+int expand_level_capacity();   // nodes the batched kernel's threshold set holds
 
 // Stage 3: mask and position ids.
 struct EmitArgs {

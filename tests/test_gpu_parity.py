@@ -141,8 +141,18 @@ def test_expand_paths_agree(name, kw, monkeypatch):
         plan = make_plan(cfg)
         outs[mode] = host(run_build(plan, lg))
     say(f"[paths] {cfg.name} n*={outs['auto']['n_star'].tolist()[:8]}")
+    _paths_agree(outs)
+
+
+def _paths_agree(outs):
+    """The two expansion kernels give the same trees; Phi (and theta from it) may differ by the
+    rounding of the summation order, far below the fp32 output precision."""
     for k, v in outs["auto"].items():
-        if v is not None:
+        if v is None:
+            continue
+        if k in ("phi", "theta"):
+            np.testing.assert_allclose(v, outs["serial"][k], rtol=1e-6, err_msg=k)
+        else:
             assert np.array_equal(v, outs["serial"][k]), k
 
 
@@ -364,9 +374,7 @@ def test_ctx_expand_paths_agree(monkeypatch):
         else:
             monkeypatch.delenv("CADDTREE_EXPAND", raising=False)
         outs[mode] = host(run_build(make_plan(cfg), lg, ctx_len=ctx))
-    for k, v in outs["auto"].items():
-        if v is not None:
-            assert np.array_equal(v, outs["serial"][k]), k
+    _paths_agree(outs)
 
 
 def test_full_c1x():
@@ -405,9 +413,7 @@ def test_fixed_budget_paths_agree(monkeypatch):
         else:
             monkeypatch.delenv("CADDTREE_EXPAND", raising=False)
         outs[mode] = host(run_build(make_plan(cfg), lg))
-    for k, v in outs["auto"].items():
-        if v is not None:
-            assert np.array_equal(v, outs["serial"][k]), k
+    _paths_agree(outs)
 
 
 def test_fixed_budget_is_top_n_of_the_greedy_tree():
