@@ -67,9 +67,12 @@ __device__ __forceinline__ int n_gen(uint32_t m) { return (int)(m >> 23); }
 
 // node a pops before node b (sigma desc, depth asc, Lambda desc, generation index asc;
 // within a depth the generation order is the rank-tuple order)
+// (branch-free: every term is evaluated, so the comparison compiles to selects)
 __device__ __forceinline__ bool pops_before(double sa, double la, uint32_t ma, double sb, double lb, uint32_t mb) {
   const int da = m_depth(ma), db = m_depth(mb);
-  return sa > sb || (sa == sb && (da < db || (da == db && (la > lb || (la == lb && n_gen(ma) < n_gen(mb))))));
+  const int t = (int)(la > lb) | ((int)(la == lb) & (int)(n_gen(ma) < n_gen(mb)));
+  const int u = (int)(da < db) | ((int)(da == db) & t);
+  return ((int)(sa > sb) | ((int)(sa == sb) & u)) != 0;
 }
 __device__ __forceinline__ bool pops_before(const Node& a, const Node& b) {
   return pops_before(a.s, a.l, a.m, b.s, b.l, b.m);
@@ -116,6 +119,13 @@ struct Cost {
   __device__ __forceinline__ double operator()(int n) const { return n < kCW ? cw[n] : C(n); }
 };
 
+// the next, lower threshold: the target, but never at or below a threshold whose
+// set overflowed (then halfway towards it)
+__device__ __forceinline__ double lower_tau(double tau, double target, double lo) {
+  if (lo > -INFINITY && !(target > lo)) return 0.5 * (tau + lo);
+  return target;
+}
+
 struct Stop {
   int n;        // first position not kept, or ns when every position is kept
   double phi;   // Phi before position n
@@ -129,11 +139,18 @@ __device__ Stop stop_small(const Lds& s, int ns, int cap, int fixed, const Cost&
   const double2 me = s.sl[i];
   const uint32_t mm = s.meta[i];
   int r = 0;
-#pragma unroll 4
-  for (int j = 0; j < ns; ++j) {
+  int j = 0;
+  for (; j + 4 <= ns; j += 4) {               // four nodes' loads in flight, then the compares
+    double2 o[4];
+    uint32_t om[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) { o[u] = s.sl[j + u]; om[u] = s.meta[j + u]; }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) r += pops_before(o[u].x, o[u].y, om[u], me.x, me.y, mm) ? 1 : 0;
+  }
+  for (; j < ns; ++j) {
     const double2 o = s.sl[j];
-    const uint32_t om = s.meta[j];
-    r += pops_before(o.x, o.y, om, me.x, me.y, mm) ? 1 : 0;
+    r += pops_before(o.x, o.y, s.meta[j], me.x, me.y, mm) ? 1 : 0;
   }
   if (live) s.dsort[r] = exp(me.x);
   __syncthreads();
@@ -317,7 +334,8 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
         int c = 0;
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          c += (live && r < K && (pv.y + (double)s.tl[d * K + (r < K ? r : 0)]) - Ad >= tau) ? 1 : 0;
+          c += (int)(r < K) & (int)((pv.y + (double)s.tl[d * K + (r < K ? r : 0)]) - Ad >= tau);
+        c = live ? c : 0;
         const int incl = wave_incl_scan(c);
         const int tot = __builtin_amdgcn_readlane(incl, kW - 1);
         const int off = incl - c;
@@ -340,7 +358,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
     cut = __ballot(cut) != 0;
     if (over) {
       lo = tau;
-      tau = hi < INFINITY ? 0.5 * (tau + hi) : tau + 1.0;
+      tau = hi < INFINITY ? 0.5 * (tau + hi) : tau + 1.5;
       tau = fmin(tau, top);
       if (!(lo < tau)) break;               // the set cannot shrink further
       continue;
@@ -348,7 +366,8 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
     ns = lb;
     if (cut && ns < need && ns < cap) {     // too few nodes to hold the stop: lower tau without selecting
       hi = tau;
-      tau = lo > -INFINITY ? 0.5 * (tau + lo) : tau - 1.5;
+      const double step = fmin(fmax(log(1.5 * (double)need / (double)(ns > 0 ? ns : 1)), 0.5), 4.0);
+      tau = lower_tau(tau, tau - step, lo);
       continue;
     }
     __syncthreads();
@@ -373,7 +392,14 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       done = true;
     } else {                                // every node kept: the stop lies below tau
       hi = tau;
-      tau = lo > -INFINITY ? 0.5 * (tau + lo) : tau - 1.5;
+      // the next pop is kept only while delta > (1 + Phi) c_{n+1} / C(n) (Lemma 1), a bound that
+      // does not fall as n grows under a convex cost: aim a little below it
+      double target = tau - 1.5;
+      if (!fixed) {
+        const double c1 = cost(ns + 1) - cost(ns);
+        if (c1 > 0.0) target = fmin(tau - 0.25, log((1.0 + st.phi) * c1 / cost(ns)) - 1.0);
+      }
+      tau = lower_tau(tau, target, lo);
     }
     if (done) theta = n == 0 ? theta0 : (1.0 + phi) / cost(n);
   }
