@@ -25,6 +25,7 @@ struct caddtree_plan {
   double* d_t_verify;   // device copy, n_ctx x (cap + 1) values
   int64_t* d_ctx_grid;  // device copy of the grid (n_ctx >= 2), else NULL
   bool use_level;       // the batched expansion applies (see plan_create)
+  int level_set_cap;    // its threshold-set capacity
   int device;
   int k1_waves;         // 0 = automatic
   int k1_unroll;        // 0 = automatic
@@ -155,6 +156,7 @@ caddtree_status_t run_expand(const caddtree_plan* p, const int32_t* ids, const f
   a.phi = phi;
   a.theta = theta;
   a.use_level = p->use_level;
+  a.level_set_cap = p->level_set_cap;
   a.fixed_budget = (p->flags & CADDTREE_FIXED_BUDGET) != 0;
   hipError_t e = caddtree::launch_expand(a, stream);
   if (e != hipSuccess) return hip_fail(e, "expand launch");
@@ -277,14 +279,14 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
   p->d_ctx_grid = nullptr;
   // The batched expansion finds the stop by bisection, which needs theta to be
   // unimodal along the pop order (a convex cost, Thm. 1), and a threshold set
-  // that holds the tree within its capacity (512 nodes): a fixed budget of at
-  // most 256 nodes, or a cost whose marginal turns positive within the first
-  // 256 nodes in every table (the tree holds at least that many nodes).
-  const int level_cap = caddtree::expand_level_capacity();
-  if (cfg->flags & CADDTREE_FIXED_BUDGET)
-    p->use_level = cap >= 1 && cap <= level_cap / 2;
-  else
-    p->use_level = cap >= 1 && convex && flat_start < level_cap / 2;
+  // that holds at least the nodes every tree keeps: the budget with a fixed
+  // budget or a cost flat up to the cap, else the nodes before the first
+  // positive marginal cost (the most over the tables).  The set is sized to
+  // twice that, 512 .. 4096 nodes.
+  const bool fixed = (cfg->flags & CADDTREE_FIXED_BUDGET) != 0;
+  const int need = (fixed || flat_start >= cap) ? cap : flat_start + 1;
+  p->use_level = cap >= 1 && (fixed || convex) && need <= caddtree::expand_level_max_need();
+  p->level_set_cap = caddtree::expand_level_set_cap(need);
   if (const char* env = std::getenv("CADDTREE_EXPAND")) {
     if (std::strcmp(env, "serial") == 0) p->use_level = false;
   }
@@ -310,6 +312,7 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
       e = hipMemcpy(p->d_ctx_grid, cfg->ctx_grid_host, sizeof(int64_t) * (size_t)J, hipMemcpyHostToDevice);
   }
   if (e == hipSuccess) e = caddtree::expand_prepare(p->L, p->K, p->cap);
+  if (e == hipSuccess) e = caddtree::expand_level_prepare();
   if (e != hipSuccess) {
     (void)hipFree(p->d_t_verify);
     if (p->d_ctx_grid) (void)hipFree(p->d_ctx_grid);

@@ -31,8 +31,9 @@
 // delta > (1 + Phi) c_{n+1} / C(n) (Lemma 1); with c_{m0+1} the first positive
 // marginal cost the stop lies past m0, around delta = (1 + Phi) c / C with Phi
 // of order one.  A round that does not settle within kMaxAttempts, or whose
-// tree needs more than kSCap nodes, is flagged (n_star = -1) and left to the
-// serial kernel, which gives the same tree.
+// tree needs more nodes than the set holds (512, or up to 4096 for fixed
+// budgets and long flat cost starts, sized by the host), is flagged
+// (n_star = -1) and left to the serial kernel, which gives the same tree.
 //
 // The kept nodes are a prefix of the pop order and a prefix-closed set, so
 // their breadth-first positions are a running count over generation order.
@@ -51,31 +52,32 @@ namespace {
 using namespace xp;
 
 constexpr int kW = 64;
-constexpr int kSCap = 512;            // nodes of T(tau) held at once
+constexpr int kSmall = 512;           // sets up to this size are selected in registers
+constexpr int kMaxSet = 4096;         // the largest set the LDS layout holds
 constexpr int kCW = 66;               // C(0 .. 65) cached in LDS
 constexpr int kMaxAttempts = 12;
 
-// One node of T(tau): sigma, Lambda, and its packed word (parent, rank, depth)
-// with the generation index in the top 9 bits.
+// One node of T(tau): sigma, Lambda, its packed word (parent, rank, depth) and
+// its generation index.
 struct Node {
   double s;
   double l;
   uint32_t m;
+  int g;
 };
-
-__device__ __forceinline__ int n_gen(uint32_t m) { return (int)(m >> 23); }
 
 // node a pops before node b (sigma desc, depth asc, Lambda desc, generation index asc;
 // within a depth the generation order is the rank-tuple order)
 // (branch-free: every term is evaluated, so the comparison compiles to selects)
-__device__ __forceinline__ bool pops_before(double sa, double la, uint32_t ma, double sb, double lb, uint32_t mb) {
+__device__ __forceinline__ bool pops_before(double sa, double la, uint32_t ma, int ga,
+                                            double sb, double lb, uint32_t mb, int gb) {
   const int da = m_depth(ma), db = m_depth(mb);
-  const int t = (int)(la > lb) | ((int)(la == lb) & (int)(n_gen(ma) < n_gen(mb)));
+  const int t = (int)(la > lb) | ((int)(la == lb) & (int)(ga < gb));
   const int u = (int)(da < db) | ((int)(da == db) & t);
   return ((int)(sa > sb) | ((int)(sa == sb) & u)) != 0;
 }
 __device__ __forceinline__ bool pops_before(const Node& a, const Node& b) {
-  return pops_before(a.s, a.l, a.m, b.s, b.l, b.m);
+  return pops_before(a.s, a.l, a.m, a.g, b.s, b.l, b.m, b.g);
 }
 
 struct Lds {
@@ -83,32 +85,33 @@ struct Lds {
   int32_t* tid;     // [L * K] token ids
   double* cw;       // [kCW] C(0 .. kCW - 1) = C_d + C_v
   double2* sl;      // T(tau) in generation order: (sigma, Lambda)
-  uint32_t* meta;   //   packed word with the generation index
-  double* dsort;    // path probabilities in pop order (small sets)
+  uint32_t* meta;   //   packed word (parent, rank, depth)
+  double* dl;       //   path probability (large sets), or in pop order (small sets)
   int16_t* pos;     // kept flag, then breadth-first position, of each node
 };
 
-__host__ __device__ __forceinline__ size_t level_lds_bytes(size_t LK) {
+// LDS of a round for a set of S nodes
+__host__ __device__ __forceinline__ size_t level_lds_bytes(size_t LK, size_t S) {
   size_t off = 0;
   off = a16(off + 4 * LK);
   off = a16(off + 4 * LK);
   off = a16(off + 8 * kCW);
-  off = a16(off + 16 * kSCap);
-  off = a16(off + 4 * kSCap);
-  off = a16(off + 8 * kW);
-  off = a16(off + 2 * kSCap);
+  off = a16(off + 16 * S);
+  off = a16(off + 4 * S);
+  off = a16(off + 8 * S);
+  off = a16(off + 2 * S);
   return off;
 }
 
-__device__ Lds carve(unsigned char* smem, size_t LK) {
+__device__ Lds carve(unsigned char* smem, size_t LK, size_t S) {
   Lds s;
   size_t off = 0;
   s.tl = reinterpret_cast<float*>(smem + off);      off = a16(off + 4 * LK);
   s.tid = reinterpret_cast<int32_t*>(smem + off);   off = a16(off + 4 * LK);
   s.cw = reinterpret_cast<double*>(smem + off);     off = a16(off + 8 * kCW);
-  s.sl = reinterpret_cast<double2*>(smem + off);    off = a16(off + 16 * kSCap);
-  s.meta = reinterpret_cast<uint32_t*>(smem + off); off = a16(off + 4 * kSCap);
-  s.dsort = reinterpret_cast<double*>(smem + off);  off = a16(off + 8 * kW);
+  s.sl = reinterpret_cast<double2*>(smem + off);    off = a16(off + 16 * S);
+  s.meta = reinterpret_cast<uint32_t*>(smem + off); off = a16(off + 4 * S);
+  s.dl = reinterpret_cast<double*>(smem + off);     off = a16(off + 8 * S);
   s.pos = reinterpret_cast<int16_t*>(smem + off);
   return s;
 }
@@ -146,15 +149,15 @@ __device__ Stop stop_small(const Lds& s, int ns, int cap, int fixed, const Cost&
 #pragma unroll
     for (int u = 0; u < 4; ++u) { o[u] = s.sl[j + u]; om[u] = s.meta[j + u]; }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) r += pops_before(o[u].x, o[u].y, om[u], me.x, me.y, mm) ? 1 : 0;
+    for (int u = 0; u < 4; ++u) r += pops_before(o[u].x, o[u].y, om[u], j + u, me.x, me.y, mm, i) ? 1 : 0;
   }
   for (; j < ns; ++j) {
     const double2 o = s.sl[j];
-    r += pops_before(o.x, o.y, s.meta[j], me.x, me.y, mm) ? 1 : 0;
+    r += pops_before(o.x, o.y, s.meta[j], j, me.x, me.y, mm, i) ? 1 : 0;
   }
-  if (live) s.dsort[r] = exp(me.x);
+  if (live) s.dl[r] = exp(me.x);
   __syncthreads();
-  const double d = lane < ns ? s.dsort[lane] : 0.0;
+  const double d = lane < ns ? s.dl[lane] : 0.0;
   const double incl = wave_incl_scan(d);
   const double pe = wave_shr1(incl);          // Phi before position `lane`
   bool keep = lane < cap;
@@ -177,15 +180,15 @@ __device__ Stop stop_large(const Lds& s, int ns, int cap, int fixed, const Cost&
     const int e = j * kW + lane;
     if (e < ns) {
       const double2 v = s.sl[e];
-      x[j] = Node{v.x, v.y, s.meta[e]};
+      x[j] = Node{v.x, v.y, s.meta[e], e};
       dl[j] = exp(v.x);
     } else {
-      x[j] = Node{-INFINITY, 0.0, (63u << 17) | ((uint32_t)e << 23)};
+      x[j] = Node{-INFINITY, 0.0, 63u << 17, e};
       dl[j] = 0.0;
     }
   }
   bool hasA = false, hasB = false;
-  Node A{0.0, 0.0, 0u}, B{0.0, 0.0, 0u};
+  Node A{0.0, 0.0, 0u, 0}, B{0.0, 0.0, 0u, 0};
   int posB = 0;
   double phiB = 0.0;
   unsigned rng = seed;
@@ -212,12 +215,14 @@ __device__ Stop stop_large(const Lds& s, int ns, int cap, int fixed, const Cost&
     }
     const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(mk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mk, 0));
     const int pl = __builtin_ctzll(__ballot(((mk >> lane) & 1ull) && below == k));
-    Node pv{0.0, 0.0, 0u};
+    Node pv{0.0, 0.0, 0u, pj * kW + pl};
     double pd = 0.0;
 #pragma unroll
     for (int j = 0; j < P; ++j)
       if (j == pj) {
-        pv = Node{rl_d(x[j].s, pl), rl_d(x[j].l, pl), rl_u(x[j].m, pl)};
+        pv.s = rl_d(x[j].s, pl);
+        pv.l = rl_d(x[j].l, pl);
+        pv.m = rl_u(x[j].m, pl);
         pd = rl_d(dl[j], pl);
       }
     int cnt = 0;
@@ -248,10 +253,79 @@ __device__ Stop stop_large(const Lds& s, int ns, int cap, int fixed, const Cost&
   return Stop{posB, phiB};
 }
 
+// sets above kSmall nodes: the same bisection with the nodes read from LDS at
+// every step
+__device__ Stop stop_lds(const Lds& s, int ns, int cap, int fixed, const Cost& cost, int lane, unsigned seed) {
+  for (int e = lane; e < ns; e += kW) s.dl[e] = exp(s.sl[e].x);
+  __syncthreads();
+  bool hasA = false, hasB = false;
+  Node A{0.0, 0.0, 0u, 0}, B{0.0, 0.0, 0u, 0};
+  int posB = 0;
+  double phiB = 0.0;
+  unsigned rng = seed;
+  // node e lies strictly between A and B in the pop order
+  auto cand = [&](int e) -> bool {
+    if (e >= ns) return false;
+    const double2 v = s.sl[e];
+    const Node x{v.x, v.y, s.meta[e], e};
+    return (!hasA || pops_before(A, x)) && (!hasB || pops_before(x, B));
+  };
+  for (;;) {
+    int total = 0;
+    for (int e0 = 0; e0 < ns; e0 += kW) total += __popcll(__ballot(cand(e0 + lane)));
+    if (total == 0) break;
+    rng = rng * 1664525u + 1013904223u;
+    int k = (int)((rng >> 8) % (unsigned)total);
+    int pe = -1;
+    for (int e0 = 0; e0 < ns && pe < 0; e0 += kW) {
+      const unsigned long long mk = __ballot(cand(e0 + lane));
+      const int c = __popcll(mk);
+      if (k < c) {
+        const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(mk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mk, 0));
+        pe = e0 + __builtin_ctzll(__ballot(((mk >> lane) & 1ull) && below == k));
+      } else {
+        k -= c;
+      }
+    }
+    const double2 pvv = s.sl[pe];
+    const Node pv{pvv.x, pvv.y, s.meta[pe], pe};
+    const double pd = s.dl[pe];
+    int cnt = 0;
+    double part = 0.0;
+    for (int e0 = 0; e0 < ns; e0 += kW) {
+      const int e = e0 + lane;
+      bool bf = false;
+      double de = 0.0;
+      if (e < ns) {
+        const double2 v = s.sl[e];
+        bf = pops_before(Node{v.x, v.y, s.meta[e], e}, pv);
+        de = s.dl[e];
+      }
+      cnt += __popcll(__ballot(bf));
+      part += bf ? de : 0.0;
+    }
+    const double ph = rl_d(wave_incl_scan(part), kW - 1);
+    bool keep = cnt < cap;
+    if (keep && !fixed) keep = (1.0 + ph + pd) / cost(cnt + 1) > (1.0 + ph) / cost(cnt);
+    if (keep) { hasA = true; A = pv; }
+    else { hasB = true; B = pv; posB = cnt; phiB = ph; }
+  }
+  if (!hasB) {
+    double part = 0.0;
+    for (int e = lane; e < ns; e += kW) part += s.dl[e];
+    return Stop{ns, rl_d(wave_incl_scan(part), kW - 1)};
+  }
+  for (int e = lane; e < ns; e += kW) {
+    const double2 v = s.sl[e];
+    s.pos[e] = pops_before(Node{v.x, v.y, s.meta[e], e}, B) ? 1 : 0;
+  }
+  return Stop{posB, phiB};
+}
+
 __global__ void __launch_bounds__(kW)
 expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict__ topk_logit,
                     const double* __restrict__ lse, int L, int K, int cap, CostTables ct, int fixed,
-                    int32_t* __restrict__ token_ids,
+                    int setcap, int32_t* __restrict__ token_ids,
                     int32_t* __restrict__ parent_out, int32_t* __restrict__ depth_out,
                     float* __restrict__ path_prob, int32_t* __restrict__ n_star_out,
                     float* __restrict__ phi_out, float* __restrict__ theta_out) {
@@ -259,7 +333,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   const int b = blockIdx.x;
   const int lane = threadIdx.x;
   const int LK = L * K;
-  const Lds s = carve(smem, (size_t)LK);
+  const Lds s = carve(smem, (size_t)LK, (size_t)setcap);
   const Cost cost{s.cw, ct.round(b)};
 
   for (int i = lane; i < LK; i += kW) {
@@ -287,19 +361,22 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   if (!fixed && cap >= 1) {
     // the first positive marginal cost c_{m0 + 1} (the stop lies past m0)
     int m0 = -1;
-    for (int i0 = 0; i0 < kSCap && i0 < cap && m0 < 0; i0 += kW) {
+    for (int i0 = 0; i0 < setcap && i0 < cap && m0 < 0; i0 += kW) {
       const int i = i0 + lane;
-      const bool up = i < cap && i < kSCap && cost(i + 1) > cost(i);
+      const bool up = i < cap && i < setcap && cost(i + 1) > cost(i);
       const unsigned long long m = __ballot(up);
       if (m) m0 = i0 + __builtin_ctzll(m);
     }
-    if (m0 < 0 || m0 >= kSCap / 2) {         // flat for too long: the serial kernel's case
-      if (lane == 0) n_star_out[b] = -1;
+    if (m0 < 0 && cap <= setcap / 2) {
+      need = cap;                           // flat up to the cap: every node is kept until the cap
+    } else if (m0 < 0 || m0 >= setcap / 2) {
+      if (lane == 0) n_star_out[b] = -1;    // flat for longer than the set holds: the serial kernel's case
       return;
+    } else {
+      need = m0 + 1;
+      const int m = m0 + 32 < cap ? m0 + 32 : cap;
+      tau = log(2.0 * (cost(m0 + 1) - cost(m0)) / cost(m)) - 0.5;
     }
-    need = m0 + 1;
-    const int m = m0 + 32 < cap ? m0 + 32 : cap;
-    tau = log(2.0 * (cost(m0 + 1) - cost(m0)) / cost(m)) - 0.5;
   } else if (fixed) {
     need = cap;
   }
@@ -318,7 +395,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       double x = 0.0, l1 = 0.0;
       if (live) { l1 = 0.0 + (double)s.tl[lane]; x = l1 - A1; }
       const bool in = live && x >= tau;     // the ranks that qualify form a prefix
-      if (in) { s.sl[lane] = make_double2(pmin(x, 0.0), l1); s.meta[lane] = pack(-1, lane, 1) | ((uint32_t)lane << 23); }
+      if (in) { s.sl[lane] = make_double2(pmin(x, 0.0), l1); s.meta[lane] = pack(-1, lane, 1); }
       ns = __popcll(__ballot(in));
       cut = ns < K;
     }
@@ -340,14 +417,14 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
         const int tot = __builtin_amdgcn_readlane(incl, kW - 1);
         const int off = incl - c;
         if (live && c < K) cut = true;
-        if (nb + tot > kSCap) { over = true; break; }
+        if (nb + tot > setcap) { over = true; break; }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           if (r < c) {
             const int i = nb + off + r;
             const double l = pv.y + (double)s.tl[d * K + r];
             s.sl[i] = make_double2(pmin(l - Ad, pv.x), l);
-            s.meta[i] = pack(p, r, d + 1) | ((uint32_t)i << 23);
+            s.meta[i] = pack(p, r, d + 1);
           }
         }
         nb += tot;
@@ -378,7 +455,8 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
     if (ns <= kW) st = stop_small(s, ns, cap, fixed, cost, lane);
     else if (ns <= 2 * kW) st = stop_large<2>(s, ns, cap, fixed, cost, lane, seed);
     else if (ns <= 4 * kW) st = stop_large<4>(s, ns, cap, fixed, cost, lane, seed);
-    else st = stop_large<8>(s, ns, cap, fixed, cost, lane, seed);
+    else if (ns <= kSmall) st = stop_large<8>(s, ns, cap, fixed, cost, lane, seed);
+    else st = stop_lds(s, ns, cap, fixed, cost, lane, seed);
 
     if (st.n < ns) {                        // the stop (or the cap) falls inside T(tau)
       n = st.n;
@@ -442,18 +520,30 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
 
 }  // namespace
 
-size_t expand_level_lds_bytes(int32_t L, int32_t K, int32_t cap) {
-  (void)cap;
-  return level_lds_bytes((size_t)L * K);
+size_t expand_level_lds_bytes(int32_t L, int32_t K, int32_t set_cap) {
+  return level_lds_bytes((size_t)L * K, (size_t)set_cap);
 }
 
-int expand_level_capacity() { return kSCap; }
+int expand_level_set_cap(int32_t need) {
+  int S = kSmall;
+  while (S < kMaxSet && S < 2 * need) S *= 2;
+  return S;
+}
+
+int expand_level_max_need() { return kMaxSet / 2; }
+
+hipError_t expand_level_prepare() {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(&expand_level_kernel),
+                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (int)level_lds_bytes((size_t)CADDTREE_MAX_L * CADDTREE_MAX_K, kMaxSet));
+}
 
 hipError_t launch_expand_level(const ExpandArgs& a, hipStream_t stream) {
   if (a.B == 0) return hipSuccess;
-  hipLaunchKernelGGL(expand_level_kernel, dim3((unsigned)a.B), dim3(kW), expand_level_lds_bytes(a.L, a.K, a.cap),
-                     stream, a.topk_ids, a.topk_logit, a.lse, a.L, a.K, a.cap, a.cost, a.fixed_budget ? 1 : 0,
-                     a.token_ids, a.parent, a.depth, a.path_prob, a.n_star, a.phi, a.theta);
+  hipLaunchKernelGGL(expand_level_kernel, dim3((unsigned)a.B), dim3(kW),
+                     expand_level_lds_bytes(a.L, a.K, a.level_set_cap), stream, a.topk_ids, a.topk_logit, a.lse,
+                     a.L, a.K, a.cap, a.cost, a.fixed_budget ? 1 : 0, a.level_set_cap, a.token_ids, a.parent,
+                     a.depth, a.path_prob, a.n_star, a.phi, a.theta);
   return hipGetLastError();
 }
 

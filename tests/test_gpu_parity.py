@@ -391,7 +391,8 @@ def test_full_c2x():
 @pytest.mark.parametrize("name,kw", [
     ("c1f16", dict(V=6000, B=8)),
     ("c1f128", dict(V=6000, B=8)),              # the batched kernel's range
-    ("c1f1024", dict(V=3000, B=3)),             # serial kernel with the LDS heap
+    ("c1f1024", dict(V=3000, B=3)),             # batched kernel, set read from LDS
+    ("c1", dict(V=2000, B=2, cap=2048, fixed=True)),   # the largest set the batched kernel holds
     ("c0", dict(fixed=True, cap=32, B=8)),      # fp32, L=4, K=4: 32 of 340 nodes
     ("c0", dict(fixed=True, L=2, K=3, cap=20, B=4, V=50)),   # 12 nodes < cap: the whole tree
 ])
