@@ -7,7 +7,8 @@
 // tile's last row) is staged in LDS; each thread produces one 32-column word of
 // one row by walking the row's ancestor chain, which is strictly decreasing in
 // the breadth-first numbering, so the walk stops as soon as it falls below the
-// word.  Packed masks store the word; dense masks expand it to bytes.
+// word.  Packed masks store the word; dense masks expand it to 32 bytes, stored
+// as two 16-byte writes where the row allows it.
 
 #include "internal.h"
 
@@ -54,7 +55,17 @@ emit_kernel(const int32_t* __restrict__ parent, const int32_t* __restrict__ dept
     } else {
       uint8_t* rowp = static_cast<uint8_t*>(mask) + (ob + i) * cap;
       const int hi = min(n, lo + 32);
-      for (int j = lo; j < hi; ++j) rowp[j] = (uint8_t)((bits >> (j - lo)) & 1u);
+      if (hi - lo == 32 && (reinterpret_cast<uintptr_t>(rowp + lo) & 15u) == 0) {
+        // 32 bytes as two 16-byte stores; (b * 0x00204081) & 0x01010101 spreads 4 bits over 4 bytes
+        uint4 q[2];
+        uint32_t* qw = reinterpret_cast<uint32_t*>(q);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) qw[k] = (((bits >> (4 * k)) & 0xFu) * 0x00204081u) & 0x01010101u;
+        reinterpret_cast<uint4*>(rowp + lo)[0] = q[0];
+        reinterpret_cast<uint4*>(rowp + lo)[1] = q[1];
+      } else {
+        for (int j = lo; j < hi; ++j) rowp[j] = (uint8_t)((bits >> (j - lo)) & 1u);
+      }
     }
   }
 }
