@@ -213,13 +213,13 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
       uint4 q[kUnroll];
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) q[u] = stream_load(p4 + ((c + u) * CH + lane * VEC) / VEC);
-      float x[kUnroll][VEC];
       float g = -INFINITY;
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        unpack(q[u], x[u]);
+      for (int u = 0; u < kUnroll; ++u) {   // unpacked twice: keeps the live registers to one chunk
+        float x[VEC];
+        unpack(q[u], x);
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) g = fmaxf(g, x[u][j]);
+        for (int j = 0; j < VEC; ++j) g = fmaxf(g, x[j]);
       }
       s.mx = wave_max(g);
       s.r = ceilf(s.mx * kLog2eHi);
@@ -231,19 +231,36 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
       for (int o = grp; o < kWave; o <<= 1) gm = fminf(gm, __shfl_xor(gm, o));
       s.thr = gm;
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) chunk_full<VEC>(s, x[u], (c + u) * CH, K);
+      for (int u = 0; u < kUnroll; ++u) {
+        float x[VEC];
+        unpack(q[u], x);
+        chunk_full<VEC>(s, x, (c + u) * CH, K);
+      }
       c += kUnroll;
     }
-    for (; c + kUnroll <= cfull; c += kUnroll) {
+    // steady state: a ring of kUnroll loads in flight; each chunk's slot is refilled with the load
+    // kUnroll chunks ahead as soon as its registers are unpacked, before its arithmetic
+    if (c + kUnroll <= cfull) {
+      const uint4* lp = p4 + lane;
       uint4 q[kUnroll];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) q[u] = stream_load(p4 + ((c + u) * CH + lane * VEC) / VEC);
+      for (int u = 0; u < kUnroll; ++u) q[u] = stream_load(lp + (int64_t)(c + u) * (CH / VEC));
+      for (; c + 2 * kUnroll <= cfull; c += kUnroll) {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          float x[VEC];
+          unpack(q[u], x);
+          q[u] = stream_load(lp + (int64_t)(c + kUnroll + u) * (CH / VEC));
+          chunk_full<VEC>(s, x, (c + u) * CH, K);
+        }
+      }
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         float x[VEC];
         unpack(q[u], x);
         chunk_full<VEC>(s, x, (c + u) * CH, K);
       }
+      c += kUnroll;
     }
     for (; c < cfull; ++c) {
       float x[VEC];
