@@ -132,7 +132,7 @@ __device__ __forceinline__ void chunk(WaveState& s, const float (&x)[VEC], unsig
   float cmax = -INFINITY;
 #pragma unroll
   for (int j = 0; j < VEC; ++j) cmax = ((ok >> j) & 1u) ? fmaxf(cmax, x[j]) : cmax;
-  if (__ballot(cmax >= s.thr)) rare<VEC>(s, x, ok, cmax, base, K);
+  if (__builtin_expect(__ballot(cmax >= s.thr) != 0, 0)) rare<VEC>(s, x, ok, cmax, base, K);
 #pragma unroll
   for (int j = 0; j < VEC; ++j) {
     const float t = term(x[j], s.r);
@@ -140,14 +140,33 @@ __device__ __forceinline__ void chunk(WaveState& s, const float (&x)[VEC], unsig
   }
 }
 
+// A full chunk.  Every lane adds its terms pairwise in fp32 and the result once in
+// fp64.  A lane whose elements include a top-K candidate (the rare path) then adds the
+// fp64 difference between its terms summed one by one and that fp32 sum, so its
+// contribution is the fp64 sum of its fp32 terms and the final fp64 correction of the
+// top-K terms removes their whole error.
 template <int VEC>
 __device__ __forceinline__ void chunk_full(WaveState& s, const float (&x)[VEC], int base, int K) {
   float cmax = x[0];
 #pragma unroll
   for (int j = 1; j < VEC; ++j) cmax = fmaxf(cmax, x[j]);
-  if (__ballot(cmax >= s.thr)) rare<VEC>(s, x, (1u << VEC) - 1u, cmax, base, K);
+  const bool cand = cmax >= s.thr;
+  const bool any = __ballot(cand) != 0;
+  if (__builtin_expect(any, 0)) rare<VEC>(s, x, (1u << VEC) - 1u, cmax, base, K);
+  float t[VEC];
 #pragma unroll
-  for (int j = 0; j < VEC; ++j) s.acc += (double)term(x[j], s.r);
+  for (int j = 0; j < VEC; ++j) t[j] = term(x[j], s.r);
+#pragma unroll
+  for (int w = 1; w < VEC; w <<= 1)
+#pragma unroll
+    for (int j = 0; j + w < VEC; j += 2 * w) t[j] += t[j + w];
+  s.acc += (double)t[0];
+  if (__builtin_expect(any, 0) && cand) {
+    double e = 0.0;
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) e += (double)term(x[j], s.r);
+    s.acc += e - (double)t[0];
+  }
 }
 
 __device__ __forceinline__ void unpack(const uint4& q, float (&x)[8]) {
@@ -241,16 +260,17 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
     // steady state: a ring of kUnroll loads in flight; each chunk's slot is refilled with the load
     // kUnroll chunks ahead as soon as its registers are unpacked, before its arithmetic
     if (c + kUnroll <= cfull) {
-      const uint4* lp = p4 + lane;
+      const uint4* lp = p4 + lane + (int64_t)c * (CH / VEC);   // chunk c of this lane
       uint4 q[kUnroll];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) q[u] = stream_load(lp + (int64_t)(c + u) * (CH / VEC));
+      for (int u = 0; u < kUnroll; ++u) q[u] = stream_load(lp + u * (CH / VEC));
       for (; c + 2 * kUnroll <= cfull; c += kUnroll) {
+        lp += kUnroll * (CH / VEC);
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
           float x[VEC];
           unpack(q[u], x);
-          q[u] = stream_load(lp + (int64_t)(c + kUnroll + u) * (CH / VEC));
+          q[u] = stream_load(lp + u * (CH / VEC));
           chunk_full<VEC>(s, x, (c + u) * CH, K);
         }
       }
@@ -270,7 +290,14 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
   }
   for (; c < c1; ++c) {   // unaligned rows, or the ragged last chunk of the row
     float x[VEC];
-    const unsigned ok = load_guarded<T, VEC>(rowp, c * CH + lane * VEC, V, x);
+    const int e = c * CH + lane * VEC;
+    unsigned ok;
+    if (kAligned && e + VEC <= V) {         // a whole vector of this lane lies in the row
+      unpack(stream_load(reinterpret_cast<const uint4*>(rowp + e)), x);
+      ok = (1u << VEC) - 1u;
+    } else {
+      ok = load_guarded<T, VEC>(rowp, e, V, x);
+    }
     chunk<VEC>(s, x, ok, c * CH, K);
   }
 
