@@ -27,7 +27,7 @@ __device__ __forceinline__ double rl_d(double v, int l) {
 }
 __device__ __forceinline__ uint32_t rl_u(uint32_t v, int l) { return (uint32_t)__builtin_amdgcn_readlane((int)v, l); }
 
-__host__ __device__ __forceinline__ size_t a16(size_t x) { return (x + 15) & ~(size_t)15; }
+__host__ __device__ constexpr size_t a16(size_t x) { return (x + 15) & ~(size_t)15; }
 
 // ---- wave scans through DPP (gfx9: row_shr within 16-lane rows, then row_bcast:15 / :31 across rows)
 template <int CTRL, int ROW_MASK, bool BOUND>

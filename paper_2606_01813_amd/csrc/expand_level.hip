@@ -8,38 +8,55 @@
 //
 //  1. build T(tau) level by level from the root.  The children of a node that
 //     reach the threshold are a prefix of its ranks (sigma falls with the rank),
-//     so each lane counts its node's children, a prefix sum gives their slots,
-//     and the set comes out in breadth-first order (depth, then rank tuple),
-//     which is also the tie-break of the pop order within a depth;
-//  2. find where the greedy stop falls along the pop order of T(tau):
-//     * up to 64 nodes: each lane ranks its node by counting the nodes that
-//       pop before it (the full order with its tie-breaks, one pass), the
-//       path probabilities are scattered into pop order, a prefix sum gives
+//     so each lane counts its node's children, stopping at the first rank that
+//     no lane takes; a prefix sum gives their slots, and the set comes out in
+//     breadth-first order (depth, then rank tuple), which is also the
+//     tie-break of the pop order within a depth.  When a level would not fit
+//     in the set, tau is raised in place: a histogram of sigma over the levels
+//     built and the candidates of the next one picks the new threshold, the
+//     set is compacted (order kept, parents renumbered), and the level is built
+//     again.  A parent's sigma is at least its children's, so what remains is
+//     T(tau') so far;
+//  2. find where the greedy stop falls along the pop order of T(tau).  Nodes
+//     that tie on sigma have the same path probability delta = exp(sigma), so
+//     Phi before every position, and with it the stop test at every position,
+//     depends only on the sigma values in descending order.  The rest of the
+//     order decides only which members are kept of a tie group that the stop
+//     cuts:
+//     * up to 64 nodes: each lane ranks its node by sigma (ties by index), the
+//       path probabilities are scattered into that order, a prefix sum gives
 //       Phi before every position m, and m is kept iff
 //       (1 + Phi_m + delta_m) / C(m + 1) > (1 + Phi_m) / C(m) and m < cap;
 //     * larger sets: under a convex cost theta rises and then falls along the
-//       pop order (Thm. 1), so "position m is kept" holds below n* and fails
-//       from n* on, and a bisection over pivot nodes finds n*: a pivot's
-//       position and the Phi before it are a count and a sum over the nodes
-//       that pop before it;
+//       pop order (Thm. 1), so "the first position holding sigma value v is
+//       kept" holds for the large values and fails for the small ones, and a
+//       bisection over the sigma values finds the last value that passes; the
+//       stop then lies inside its tie group, whose positions are tested in
+//       parallel;
 //     with a fixed budget m is kept iff m < cap;
 //  3. if every node of T(tau) is kept and the tree continues below tau, lower
-//     tau and start again; if T(tau) outgrows its capacity, raise tau
-//     (bisection between the two).
+//     tau and start again; likewise when T(tau) holds fewer nodes than every
+//     tree keeps (a flat start of the cost, or a fixed budget).
 //
 // The initial tau comes from the cost model: a node kept near position n has
 // delta > (1 + Phi) c_{n+1} / C(n) (Lemma 1); with c_{m0+1} the first positive
 // marginal cost the stop lies past m0, around delta = (1 + Phi) c / C with Phi
-// of order one.  A round that does not settle within kMaxAttempts, or whose
-// tree needs more nodes than the set holds (512, or up to 4096 for fixed
-// budgets and long flat cost starts, sized by the host), is flagged
-// (n_star = -1) and left to the serial kernel, which gives the same tree.
+// of order one.  Flat starts and fixed budgets, which keep a known number of
+// nodes, start well below and let the in-place raise bring the set to size.
+// A round that does not settle within kMaxAttempts (or kMaxRaises raises in
+// one attempt), or whose tree needs more nodes than the set holds (512, or up
+// to 4096 for fixed budgets and long flat cost starts, sized by the host), is
+// flagged (n_star = -1) and left to the serial kernel, which gives the same
+// tree.
 //
 // The kept nodes are a prefix of the pop order and a prefix-closed set, so
 // their breadth-first positions are a running count over generation order.
 // Phi here is a prefix sum over the wave rather than a left-to-right sum in
 // pop order: it matches the sequential sum to rounding, and the tree does not
 // depend on it except at stop margins of that size.
+//
+// The workgroup is a single wavefront, whose LDS operations complete in issue
+// order, so what one step writes to LDS the next step reads without a barrier.
 
 #include <cmath>
 
@@ -54,17 +71,22 @@ using namespace xp;
 constexpr int kW = 64;
 constexpr int kSmall = 512;           // sets up to this size are selected in registers
 constexpr int kMaxSet = 4096;         // the largest set the LDS layout holds
-constexpr int kCW = 66;               // C(0 .. 65) cached in LDS
 constexpr int kMaxAttempts = 12;
+constexpr int kBins = kW;             // histogram bins of the in-place raise (one per lane)
+constexpr int kRefine = 4;            // histogram passes per raise
+constexpr int kMaxRaises = 32;        // raises per attempt
+constexpr double kDropFlat = 3.0;     // a flat start begins this far (nats) below the cost-model threshold
 
-// One node of T(tau): sigma, Lambda, its packed word (parent, rank, depth) and
-// its generation index.
-struct Node {
-  double s;
-  double l;
-  uint32_t m;
-  int g;
-};
+// Fixed budgets and costs flat up to the cap keep `need` nodes: the first threshold lies this far
+// (nats) below the top node, further for larger trees.
+__device__ __forceinline__ double drop_fixed(int need) {
+  const double d = 6.0 + 2.0 * log2((double)(need > 128 ? need : 128) / 128.0);
+  return d < 12.0 ? d : 12.0;
+}
+
+__device__ __forceinline__ int lane_below(unsigned long long m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+}
 
 // node a pops before node b (sigma desc, depth asc, Lambda desc, generation index asc;
 // within a depth the generation order is the rank-tuple order)
@@ -76,130 +98,194 @@ __device__ __forceinline__ bool pops_before(double sa, double la, uint32_t ma, i
   const int u = (int)(da < db) | ((int)(da == db) & t);
   return ((int)(sa > sb) | ((int)(sa == sb) & u)) != 0;
 }
-__device__ __forceinline__ bool pops_before(const Node& a, const Node& b) {
-  return pops_before(a.s, a.l, a.m, a.g, b.s, b.l, b.m, b.g);
-}
 
 struct Lds {
   float* tl;        // [L * K] raw logits
   int32_t* tid;     // [L * K] token ids
-  double* cw;       // [kCW] C(0 .. kCW - 1) = C_d + C_v
-  double2* sl;      // T(tau) in generation order: (sigma, Lambda)
-  uint32_t* meta;   //   packed word (parent, rank, depth)
-  double* dl;       //   path probability (large sets), or in pop order (small sets)
-  int16_t* pos;     // kept flag, then breadth-first position, of each node
+  double* cw;       // [S + 2] C(n) = C_d + C_v(min(n, cap)), for costs other than fixed budgets
+  double2* sl;      // [S] T(tau) in generation order: (sigma, Lambda)
+  uint32_t* meta;   // [S]   packed word (parent, rank, depth)
+  double* dl;       // [S]   path probability (sets above kSmall), or in sigma order (small sets)
+  int16_t* pos;     // [S]   new index (raise), kept flag, then breadth-first position
+  int* hist;        // [kBins]
 };
 
 // LDS of a round for a set of S nodes
-__host__ __device__ __forceinline__ size_t level_lds_bytes(size_t LK, size_t S) {
-  size_t off = 0;
-  off = a16(off + 4 * LK);
-  off = a16(off + 4 * LK);
-  off = a16(off + 8 * kCW);
-  off = a16(off + 16 * S);
-  off = a16(off + 4 * S);
-  off = a16(off + 8 * S);
-  off = a16(off + 2 * S);
-  return off;
+__host__ __device__ constexpr size_t level_lds_bytes(size_t LK, size_t S) {
+  return a16(a16(a16(a16(a16(a16(a16(a16(4 * LK) + 4 * LK) + 8 * (S + 2)) + 16 * S) + 4 * S) + 8 * S) + 2 * S) +
+             4 * (size_t)kBins);
 }
+static_assert(level_lds_bytes((size_t)CADDTREE_MAX_L * CADDTREE_MAX_K, kMaxSet) <= 160 * 1024,
+              "the largest set must fit in the LDS of one CU");
 
 __device__ Lds carve(unsigned char* smem, size_t LK, size_t S) {
   Lds s;
   size_t off = 0;
   s.tl = reinterpret_cast<float*>(smem + off);      off = a16(off + 4 * LK);
   s.tid = reinterpret_cast<int32_t*>(smem + off);   off = a16(off + 4 * LK);
-  s.cw = reinterpret_cast<double*>(smem + off);     off = a16(off + 8 * kCW);
+  s.cw = reinterpret_cast<double*>(smem + off);     off = a16(off + 8 * (S + 2));
   s.sl = reinterpret_cast<double2*>(smem + off);    off = a16(off + 16 * S);
   s.meta = reinterpret_cast<uint32_t*>(smem + off); off = a16(off + 4 * S);
   s.dl = reinterpret_cast<double*>(smem + off);     off = a16(off + 8 * S);
-  s.pos = reinterpret_cast<int16_t*>(smem + off);
+  s.pos = reinterpret_cast<int16_t*>(smem + off);   off = a16(off + 2 * S);
+  s.hist = reinterpret_cast<int*>(smem + off);
   return s;
 }
 
-struct Cost {
-  const double* cw;
-  RoundCost C;
-  __device__ __forceinline__ double operator()(int n) const { return n < kCW ? cw[n] : C(n); }
+// The cost table C(0 .. ncw - 1) in LDS is filled on demand, 64 entries at a time, so a round
+// reads from HBM (or L2) only the part of the table that its positions reach.
+struct CostCache {
+  const RoundCost rc;
+  double* cw;
+  int cap;
+  int ncw;       // entries the table holds at most
+  int filled;    // entries written so far (wave-uniform)
+
+  // make C(0 .. k - 1) available
+  __device__ __forceinline__ void ensure(int k, int lane) {
+    if (k > ncw) k = ncw;
+    if (k <= filled) return;
+    constexpr int kC = 8;                    // entries per lane and batch
+    const int hi = ((k + kW - 1) / kW) * kW < ncw ? ((k + kW - 1) / kW) * kW : ncw;
+    for (int i0 = filled; i0 < hi; i0 += kC * kW) {
+      double cv[kC];
+      int ci[kC];
+#pragma unroll
+      for (int u = 0; u < kC; ++u) {        // clamped, not guarded, so the loads go out together;
+        ci[u] = i0 + u * kW + lane < hi ? i0 + u * kW + lane : hi - 1;   // past the end, every
+        cv[u] = rc(ci[u] < cap ? ci[u] : cap);                             // lane reads one entry
+      }
+#pragma unroll
+      for (int u = 0; u < kC; ++u) cw[ci[u]] = cv[u];
+    }
+    filled = hi;
+  }
 };
 
-// the next, lower threshold: the target, but never at or below a threshold whose
-// set overflowed (then halfway towards it)
-__device__ __forceinline__ double lower_tau(double tau, double target, double lo) {
-  if (lo > -INFINITY && !(target > lo)) return 0.5 * (tau + lo);
-  return target;
+// position m of the pop order is kept, with Phi before it and delta at it
+__device__ __forceinline__ bool kept_at(int m, double phi, double delta, int cap, int fixed, const double* cw) {
+  if (m >= cap) return false;
+  if (fixed) return true;
+  return (1.0 + phi + delta) / cw[m + 1] > (1.0 + phi) / cw[m];
 }
 
 struct Stop {
   int n;        // first position not kept, or ns when every position is kept
   double phi;   // Phi before position n
+  bool all;     // every position is kept (no flags written)
 };
 
-// up to 64 nodes: rank by counting, Phi by a prefix sum over pop positions;
-// on a stop inside the set, the kept flags go to s.pos by generation index
-__device__ Stop stop_small(const Lds& s, int ns, int cap, int fixed, const Cost& cost, int lane) {
-  const bool live = lane < ns;
-  const int i = live ? lane : 0;
-  const double2 me = s.sl[i];
-  const uint32_t mm = s.meta[i];
-  int r = 0;
-  int j = 0;
-  for (; j + 4 <= ns; j += 4) {               // four nodes' loads in flight, then the compares
-    double2 o[4];
-    uint32_t om[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) { o[u] = s.sl[j + u]; om[u] = s.meta[j + u]; }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) r += pops_before(o[u].x, o[u].y, om[u], j + u, me.x, me.y, mm, i) ? 1 : 0;
-  }
-  for (; j < ns; ++j) {
-    const double2 o = s.sl[j];
-    r += pops_before(o.x, o.y, s.meta[j], j, me.x, me.y, mm, i) ? 1 : 0;
-  }
-  if (live) s.dl[r] = exp(me.x);
-  __syncthreads();
-  const double d = lane < ns ? s.dl[lane] : 0.0;
-  const double incl = wave_incl_scan(d);
-  const double pe = wave_shr1(incl);          // Phi before position `lane`
-  bool keep = lane < cap;
-  if (keep && !fixed && lane < ns) keep = (1.0 + pe + d) / cost(lane + 1) > (1.0 + pe) / cost(lane);
-  const unsigned long long fm = __ballot(lane < ns && !keep);
-  if (!fm) return Stop{ns, rl_d(incl, kW - 1)};
-  const int stop = __builtin_ctzll(fm);
-  if (live) s.pos[lane] = r < stop ? 1 : 0;
-  return Stop{stop, rl_d(pe, stop)};
-}
-
-// larger sets: bisection over pivots (P nodes per lane, position e = j * 64 + lane
-// in generation order)
+// Kept flags when the stop cuts a tie group: the group (sigma == v) fills pop positions
+// [g0, g0 + t), and its members at positions below `stop` are kept.  A member's position
+// is g0 plus the number of members that pop before it; the members are walked one by
+// one (as many steps as the group has members), each against every lane's nodes.
 template <int P>
-__device__ Stop stop_large(const Lds& s, int ns, int cap, int fixed, const Cost& cost, int lane, unsigned seed) {
-  Node x[P];
-  double dl[P];
+__device__ void cut_group_flags(const Lds& s, int ns, const double (&sg)[P], double v, int g0, int stop, int lane) {
+  int rt[P];
+  double lam[P];
+  uint32_t mm[P];
 #pragma unroll
   for (int j = 0; j < P; ++j) {
     const int e = j * kW + lane;
-    if (e < ns) {
-      const double2 v = s.sl[e];
-      x[j] = Node{v.x, v.y, s.meta[e], e};
-      dl[j] = exp(v.x);
-    } else {
-      x[j] = Node{-INFINITY, 0.0, 63u << 17, e};
-      dl[j] = 0.0;
+    rt[j] = 0;
+    lam[j] = e < ns ? s.sl[e].y : 0.0;
+    mm[j] = e < ns ? s.meta[e] : 0u;
+  }
+#pragma unroll
+  for (int jo = 0; jo < P; ++jo) {
+    unsigned long long gm = __ballot(jo * kW + lane < ns && sg[jo] == v);
+    while (gm) {
+      const int ol = __builtin_ctzll(gm);
+      gm &= gm - 1;
+      const int o = jo * kW + ol;
+      const double lo = rl_d(lam[jo], ol);
+      const uint32_t mo = rl_u(mm[jo], ol);
+#pragma unroll
+      for (int j = 0; j < P; ++j)
+        rt[j] += (sg[j] == v && pops_before(v, lo, mo, o, v, lam[j], mm[j], j * kW + lane)) ? 1 : 0;
     }
   }
+#pragma unroll
+  for (int j = 0; j < P; ++j) {
+    const int e = j * kW + lane;
+    if (e < ns) s.pos[e] = (sg[j] > v || (sg[j] == v && g0 + rt[j] < stop)) ? 1 : 0;
+  }
+}
+
+// up to 64 nodes: rank by sigma (ties by index), Phi by a prefix sum over those positions;
+// on a stop inside the set, the kept flags go to s.pos by generation index
+__device__ Stop stop_small(const Lds& s, int ns, int cap, int fixed, int lane) {
+  const bool live = lane < ns;
+  double sg[1];
+  sg[0] = live ? s.sl[lane].x : -INFINITY;
+  const double me = sg[0];
+  int r = 0;
+  int o = 0;
+  for (; o + 4 <= ns; o += 4) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const double so = rl_d(me, o + u);
+      r += (int)(so > me) | ((int)(so == me) & (int)(o + u < lane));
+    }
+  }
+  for (; o < ns; ++o) {
+    const double so = rl_d(me, o);
+    r += (int)(so > me) | ((int)(so == me) & (int)(o < lane));
+  }
+  if (live) s.dl[r] = exp(me);
+  const double d = live ? s.dl[lane] : 0.0;   // delta at position `lane`
+  const double incl = wave_incl_scan(d);
+  const double pe = wave_shr1(incl);          // Phi before position `lane`
+  const bool keep = live && kept_at(lane, pe, d, cap, fixed, s.cw);
+  const unsigned long long fm = __ballot(live && !keep);
+  if (!fm) return Stop{ns, rl_d(incl, kW - 1), true};
+  const int stop = __builtin_ctzll(fm);
+  // the tie group at the stop position
+  const double v = rl_d(me, __builtin_ctzll(__ballot(live && r == stop)));
+  const int g0 = __popcll(__ballot(live && me > v));
+  if (g0 < stop) {
+    cut_group_flags<1>(s, ns, sg, v, g0, stop, lane);
+  } else if (live) {
+    s.pos[lane] = me > v ? 1 : 0;
+  }
+  return Stop{stop, rl_d(pe, stop), false};
+}
+
+// The stop inside the tie group of value vA (first position mA, Phi before it phA, delta dA,
+// tA members): the offset of the first member position that is not kept, or tA.
+__device__ __forceinline__ int group_stop(int mA, double phA, double dA, int tA, int cap, int fixed,
+                                          const double* cw, int lane) {
+  for (int k0 = 1; k0 < tA; k0 += kW) {
+    const int k = k0 + lane;
+    const bool bad = k < tA && !kept_at(mA + k, phA + (double)k * dA, dA, cap, fixed, cw);
+    const unsigned long long bm = __ballot(bad);
+    if (bm) return k0 + __builtin_ctzll(bm);
+  }
+  return tA;
+}
+
+// larger sets held in registers: P sigma values per lane, node e = j * 64 + lane
+template <int P>
+__device__ Stop stop_reg(const Lds& s, int ns, int cap, int fixed, int lane, unsigned seed) {
+  double sg[P], dl[P];
+#pragma unroll
+  for (int j = 0; j < P; ++j) {
+    const int e = j * kW + lane;
+    sg[j] = e < ns ? s.sl[e].x : -INFINITY;
+    dl[j] = e < ns ? exp(sg[j]) : 0.0;
+  }
+  // bisection over the sigma values: vA is the smallest value seen whose first position is
+  // kept, vB the largest value seen whose first position is not
   bool hasA = false, hasB = false;
-  Node A{0.0, 0.0, 0u, 0}, B{0.0, 0.0, 0u, 0};
-  int posB = 0;
-  double phiB = 0.0;
+  double vA = 0.0, vB = 0.0, dA = 0.0, phA = 0.0;
+  int mA = 0;
   unsigned rng = seed;
   for (;;) {
     unsigned long long cm[P];
     int total = 0;
 #pragma unroll
     for (int j = 0; j < P; ++j) {
-      bool c = j * kW + lane < ns;
-      if (hasA) c = c && pops_before(A, x[j]);
-      if (hasB) c = c && pops_before(x[j], B);
+      const bool c = j * kW + lane < ns && (!hasA || sg[j] < vA) && (!hasB || sg[j] > vB);
       cm[j] = __ballot(c);
       total += __popcll(cm[j]);
     }
@@ -213,62 +299,57 @@ __device__ Stop stop_large(const Lds& s, int ns, int cap, int fixed, const Cost&
       const int c = __popcll(cm[j]);
       if (pj == j && k >= c) { k -= c; pj = j + 1; mk = cm[j + 1]; }
     }
-    const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(mk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mk, 0));
-    const int pl = __builtin_ctzll(__ballot(((mk >> lane) & 1ull) && below == k));
-    Node pv{0.0, 0.0, 0u, pj * kW + pl};
-    double pd = 0.0;
+    const int pl = __builtin_ctzll(__ballot(((mk >> lane) & 1ull) && lane_below(mk) == k));
+    double v = 0.0, pd = 0.0;
 #pragma unroll
     for (int j = 0; j < P; ++j)
-      if (j == pj) {
-        pv.s = rl_d(x[j].s, pl);
-        pv.l = rl_d(x[j].l, pl);
-        pv.m = rl_u(x[j].m, pl);
-        pd = rl_d(dl[j], pl);
-      }
+      if (j == pj) { v = rl_d(sg[j], pl); pd = rl_d(dl[j], pl); }
     int cnt = 0;
     double part = 0.0;
 #pragma unroll
     for (int j = 0; j < P; ++j) {
-      const bool bf = j * kW + lane < ns && pops_before(x[j], pv);
+      const bool bf = sg[j] > v;
       cnt += __popcll(__ballot(bf));
       part += bf ? dl[j] : 0.0;
     }
     const double ph = rl_d(wave_incl_scan(part), kW - 1);
-    bool keep = cnt < cap;
-    if (keep && !fixed) keep = (1.0 + ph + pd) / cost(cnt + 1) > (1.0 + ph) / cost(cnt);
-    if (keep) { hasA = true; A = pv; }
-    else { hasB = true; B = pv; posB = cnt; phiB = ph; }
+    if (kept_at(cnt, ph, pd, cap, fixed, s.cw)) { hasA = true; vA = v; dA = pd; mA = cnt; phA = ph; }
+    else { hasB = true; vB = v; }
   }
-  if (!hasB) {
-    double part = 0.0;
+  if (!hasA) {                                // not even the first position is kept
 #pragma unroll
-    for (int j = 0; j < P; ++j) part += dl[j];
-    return Stop{ns, rl_d(wave_incl_scan(part), kW - 1)};
+    for (int j = 0; j < P; ++j)
+      if (j * kW + lane < ns) s.pos[j * kW + lane] = 0;
+    return Stop{0, 0.0, false};
   }
+  int tA = 0;
 #pragma unroll
-  for (int j = 0; j < P; ++j) {
-    const int e = j * kW + lane;
-    if (e < ns) s.pos[e] = pops_before(x[j], B) ? 1 : 0;
+  for (int j = 0; j < P; ++j) tA += __popcll(__ballot(j * kW + lane < ns && sg[j] == vA));
+  const int ks = group_stop(mA, phA, dA, tA, cap, fixed, s.cw, lane);
+  const int n = mA + ks;
+  const double phi = phA + (double)ks * dA;
+  if (n == ns) return Stop{ns, phi, true};
+  if (ks < tA) {
+    cut_group_flags<P>(s, ns, sg, vA, mA, n, lane);
+  } else {
+#pragma unroll
+    for (int j = 0; j < P; ++j)
+      if (j * kW + lane < ns) s.pos[j * kW + lane] = sg[j] >= vA ? 1 : 0;
   }
-  return Stop{posB, phiB};
+  return Stop{n, phi, false};
 }
 
-// sets above kSmall nodes: the same bisection with the nodes read from LDS at
-// every step
-__device__ Stop stop_lds(const Lds& s, int ns, int cap, int fixed, const Cost& cost, int lane, unsigned seed) {
+// sets above kSmall nodes: the same bisection with the values read from LDS at every step
+__device__ Stop stop_lds(const Lds& s, int ns, int cap, int fixed, int lane, unsigned seed) {
   for (int e = lane; e < ns; e += kW) s.dl[e] = exp(s.sl[e].x);
-  __syncthreads();
   bool hasA = false, hasB = false;
-  Node A{0.0, 0.0, 0u, 0}, B{0.0, 0.0, 0u, 0};
-  int posB = 0;
-  double phiB = 0.0;
+  double vA = 0.0, vB = 0.0, dA = 0.0, phA = 0.0;
+  int mA = 0;
   unsigned rng = seed;
-  // node e lies strictly between A and B in the pop order
   auto cand = [&](int e) -> bool {
     if (e >= ns) return false;
-    const double2 v = s.sl[e];
-    const Node x{v.x, v.y, s.meta[e], e};
-    return (!hasA || pops_before(A, x)) && (!hasB || pops_before(x, B));
+    const double x = s.sl[e].x;
+    return (!hasA || x < vA) && (!hasB || x > vB);
   };
   for (;;) {
     int total = 0;
@@ -280,46 +361,156 @@ __device__ Stop stop_lds(const Lds& s, int ns, int cap, int fixed, const Cost& c
     for (int e0 = 0; e0 < ns && pe < 0; e0 += kW) {
       const unsigned long long mk = __ballot(cand(e0 + lane));
       const int c = __popcll(mk);
-      if (k < c) {
-        const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(mk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mk, 0));
-        pe = e0 + __builtin_ctzll(__ballot(((mk >> lane) & 1ull) && below == k));
-      } else {
-        k -= c;
-      }
+      if (k < c) pe = e0 + __builtin_ctzll(__ballot(((mk >> lane) & 1ull) && lane_below(mk) == k));
+      else k -= c;
     }
-    const double2 pvv = s.sl[pe];
-    const Node pv{pvv.x, pvv.y, s.meta[pe], pe};
+    const double v = s.sl[pe].x;
     const double pd = s.dl[pe];
     int cnt = 0;
     double part = 0.0;
     for (int e0 = 0; e0 < ns; e0 += kW) {
       const int e = e0 + lane;
-      bool bf = false;
-      double de = 0.0;
-      if (e < ns) {
-        const double2 v = s.sl[e];
-        bf = pops_before(Node{v.x, v.y, s.meta[e], e}, pv);
-        de = s.dl[e];
-      }
+      const bool bf = e < ns && s.sl[e].x > v;
       cnt += __popcll(__ballot(bf));
-      part += bf ? de : 0.0;
+      part += bf ? s.dl[e] : 0.0;
     }
     const double ph = rl_d(wave_incl_scan(part), kW - 1);
-    bool keep = cnt < cap;
-    if (keep && !fixed) keep = (1.0 + ph + pd) / cost(cnt + 1) > (1.0 + ph) / cost(cnt);
-    if (keep) { hasA = true; A = pv; }
-    else { hasB = true; B = pv; posB = cnt; phiB = ph; }
+    if (kept_at(cnt, ph, pd, cap, fixed, s.cw)) { hasA = true; vA = v; dA = pd; mA = cnt; phA = ph; }
+    else { hasB = true; vB = v; }
   }
-  if (!hasB) {
-    double part = 0.0;
-    for (int e = lane; e < ns; e += kW) part += s.dl[e];
-    return Stop{ns, rl_d(wave_incl_scan(part), kW - 1)};
+  if (!hasA) {
+    for (int e = lane; e < ns; e += kW) s.pos[e] = 0;
+    return Stop{0, 0.0, false};
   }
-  for (int e = lane; e < ns; e += kW) {
-    const double2 v = s.sl[e];
-    s.pos[e] = pops_before(Node{v.x, v.y, s.meta[e], e}, B) ? 1 : 0;
+  int tA = 0;
+  for (int e0 = 0; e0 < ns; e0 += kW) {
+    const int e = e0 + lane;
+    tA += __popcll(__ballot(e < ns && s.sl[e < ns ? e : 0].x == vA));
   }
-  return Stop{posB, phiB};
+  const int ks = group_stop(mA, phA, dA, tA, cap, fixed, s.cw, lane);
+  const int n = mA + ks;
+  const double phi = phA + (double)ks * dA;
+  if (n == ns) return Stop{ns, phi, true};
+  if (ks == tA) {
+    for (int e = lane; e < ns; e += kW) s.pos[e] = s.sl[e].x >= vA ? 1 : 0;
+    return Stop{n, phi, false};
+  }
+  // the stop cuts the group of vA: list its members (generation order) in the dl array, which
+  // the bisection no longer needs, then rank each member by the members that pop before it
+  int* mem = reinterpret_cast<int*>(s.dl);
+  int t = 0;
+  for (int e0 = 0; e0 < ns; e0 += kW) {
+    const int e = e0 + lane;
+    const bool g = e < ns && s.sl[e < ns ? e : 0].x == vA;
+    const unsigned long long gm = __ballot(g);
+    if (g) mem[t + lane_below(gm)] = e;
+    t += __popcll(gm);
+  }
+  for (int e = lane; e < ns; e += kW) s.pos[e] = s.sl[e].x > vA ? 1 : 0;
+  for (int j0 = 0; j0 < t; j0 += kW) {         // 64 members at a time ...
+    const int j = j0 + lane;
+    const bool live = j < t;
+    const int e = mem[live ? j : 0];
+    const double lam = s.sl[e].y;
+    const uint32_t mme = s.meta[e];
+    int rt = 0;
+    for (int q0 = 0; q0 < t; q0 += kW) {        // ... against every member, 64 at a time
+      const int q = q0 + lane;
+      const int eo = mem[q < t ? q : 0];
+      const double lo = s.sl[eo].y;
+      const uint32_t mo = s.meta[eo];
+      const int nq = t - q0 < kW ? t - q0 : kW;
+      for (int k = 0; k < nq; ++k)
+        rt += pops_before(vA, rl_d(lo, k), rl_u(mo, k), __builtin_amdgcn_readlane(eo, k), vA, lam, mme, e) ? 1 : 0;
+    }
+    if (live) s.pos[e] = mA + rt < n ? 1 : 0;
+  }
+  return Stop{n, phi, false};
+}
+
+// Raise tau in place at depth d.  Depths 1 .. d are s[0, lb) (depth d at [la, lb)); the
+// children of depth d that reach tau are the candidates at depth d + 1.  Picks tau' > tau
+// such that T(tau') over depths 1 .. d + 1 holds at most keep_hi nodes and, as far as the
+// histogram resolves, at least `need`; compacts s[0, lb) to the nodes that reach tau'
+// (order kept, parents renumbered) and updates la, lb.  Returns tau', or NaN when no such
+// threshold is found.
+__device__ double raise_tau(const Lds& s, int& la, int& lb, int K, double Ad, double tlv, double tau, double top,
+                            int keep_hi, int need, int lane) {
+  double lo_e = tau, hi_e = top;
+  int above = 0;                             // nodes above the histogram's range
+  double t2 = NAN;
+  for (int pass = 0; pass < kRefine; ++pass) {
+    if (!(hi_e > lo_e)) break;
+    const double scale = (double)kBins / (hi_e - lo_e);
+    const bool first = pass == 0;            // the first pass also takes the values at hi_e
+    auto bin = [&](double v) -> int {
+      const int b = (int)((v - lo_e) * scale);
+      return b < kBins - 1 ? b : kBins - 1;
+    };
+    s.hist[lane] = 0;
+    for (int i0 = 0; i0 < lb; i0 += kW) {
+      const int i = i0 + lane;
+      if (i < lb) {
+        const double v = s.sl[i].x;
+        if (v >= lo_e && (first || v < hi_e)) atomicAdd(&s.hist[bin(v)], 1);
+      }
+    }
+    for (int p0 = la; p0 < lb; p0 += kW) {
+      const int p = p0 + lane;
+      const bool live = p < lb;
+      const double2 pv = s.sl[live ? p : la];
+      for (int r = 0; r < K; ++r) {
+        const double x = (pv.y + rl_d(tlv, r)) - Ad;
+        const bool q = live && x >= tau;
+        if (__ballot(q) == 0) break;
+        if (q) {
+          const double v = pmin(x, pv.x);
+          if (v >= lo_e && (first || v < hi_e)) atomicAdd(&s.hist[bin(v)], 1);
+        }
+      }
+    }
+    const int h = s.hist[lane];
+    const int incl = wave_incl_scan(h);
+    const int tot = __builtin_amdgcn_readlane(incl, kW - 1);
+    const int S = above + tot - (incl - h);   // nodes in bins >= lane, and above the range
+    const unsigned long long okm = __ballot(S <= keep_hi);
+    const int b1 = okm ? __builtin_ctzll(okm) : kBins;
+    const int S1 = b1 < kBins ? __builtin_amdgcn_readlane(S, b1) : above;
+    if (b1 == 0) break;                       // everything fits: nothing to raise
+    if (S1 >= need) {
+      t2 = lo_e + (hi_e - lo_e) * ((double)b1 / (double)kBins);
+      break;
+    }
+    // bin b1 - 1 holds both bounds: split it
+    above = S1;
+    const double w = (hi_e - lo_e) / (double)kBins;
+    hi_e = lo_e + w * (double)b1;
+    lo_e = lo_e + w * (double)(b1 - 1);
+  }
+  if (!(t2 > tau)) return NAN;
+  // compact s[0, lb) to the nodes with sigma >= t2
+  int base = 0, la2 = 0;
+  for (int i0 = 0; i0 < lb; i0 += kW) {
+    const int i = i0 + lane;
+    const bool live = i < lb;
+    const double2 v = s.sl[live ? i : 0];
+    const uint32_t m = s.meta[live ? i : 0];
+    const bool keep = live && v.x >= t2;
+    const unsigned long long km = __ballot(keep);
+    const int j = base + lane_below(km);
+    if (live) s.pos[i] = keep ? (int16_t)j : (int16_t)-1;
+    const int par = m_parent(m);
+    const int np = (keep && par >= 0) ? (int)s.pos[par] : -1;   // parents come first and are kept
+    if (keep) {
+      s.sl[j] = v;
+      s.meta[j] = pack(np, m_rank(m), m_depth(m));
+    }
+    if (la >= i0 && la < i0 + kW) la2 = base + __popcll(km & ((1ull << (la - i0)) - 1ull));
+    base += __popcll(km);
+  }
+  la = la2;
+  lb = base;
+  return t2;
 }
 
 __global__ void __launch_bounds__(kW)
@@ -334,15 +525,33 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   const int lane = threadIdx.x;
   const int LK = L * K;
   const Lds s = carve(smem, (size_t)LK, (size_t)setcap);
-  const Cost cost{s.cw, ct.round(b)};
+  const RoundCost rc = ct.round(b);
 
-  for (int i = lane; i < LK; i += kW) {
-    s.tl[i] = topk_logit[(int64_t)b * LK + i];
-    s.tid[i] = topk_ids[(int64_t)b * LK + i];
+  // setup: the round's global loads are issued together, then stored to LDS.  Indices are
+  // clamped rather than guarded (a clamped lane loads and stores the same value as the last
+  // valid one), so neither loads nor stores sit behind branches.
+  const double c0 = rc(0);
+  const double lse_l = lse[(int64_t)b * L + (lane < L ? lane : L - 1)];
+  CostCache cc{rc, s.cw, cap, fixed ? 0 : (cap < setcap ? cap : setcap) + 2, 0};   // C(0 .. ncw - 1)
+  {
+    constexpr int kT = CADDTREE_MAX_L * CADDTREE_MAX_K / kW;        // top-K entries per lane, at most
+    float lv[kT];
+    int32_t iv[kT];
+#pragma unroll
+    for (int u = 0; u < kT; ++u) {          // clamped like the cost table
+      const int i = u * kW + lane < LK ? u * kW + lane : LK - 1;
+      lv[u] = topk_logit[(int64_t)b * LK + i];
+      iv[u] = topk_ids[(int64_t)b * LK + i];
+    }
+    cc.ensure(kW + 2, lane);
+#pragma unroll
+    for (int u = 0; u < kT; ++u) {
+      const int i = u * kW + lane < LK ? u * kW + lane : LK - 1;
+      s.tl[i] = lv[u];
+      s.tid[i] = iv[u];
+    }
   }
-  for (int i = lane; i < kCW; i += kW) s.cw[i] = i <= cap ? cost.C(i) : 1.0;
   // lane d holds A_d = sum_{i<=d} LSE_i, summed in depth order (d = 0 .. L)
-  const double lse_l = lane < L ? lse[(int64_t)b * L + lane] : 0.0;
   double Areg = 0.0;
   {
     double acc = 0.0;
@@ -353,43 +562,64 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   }
   __syncthreads();
 
-  const double theta0 = 1.0 / s.cw[0];
+  const double theta0 = 1.0 / c0;
   const double A1 = rl_d(Areg, 1);
   const double top = pmin(0.0 + (double)s.tl[0] - A1, 0.0);   // the first node to pop
   double tau = top - 3.0;
   int need = 1;                              // the tree holds at least this many nodes
-  if (!fixed && cap >= 1) {
+  bool tight = false;                        // need is what the tree keeps before any stop test
+  if (fixed) {
+    need = cap;
+    tight = true;
+    tau = top - drop_fixed(need);
+  } else if (cap >= 1) {
     // the first positive marginal cost c_{m0 + 1} (the stop lies past m0)
     int m0 = -1;
-    for (int i0 = 0; i0 < setcap && i0 < cap && m0 < 0; i0 += kW) {
+    const int mlim = cap < setcap ? cap : setcap;
+    for (int i0 = 0; i0 < mlim && m0 < 0; i0 += kW) {
       const int i = i0 + lane;
-      const bool up = i < cap && i < setcap && cost(i + 1) > cost(i);
-      const unsigned long long m = __ballot(up);
+      cc.ensure(i0 + kW + 1, lane);
+      const unsigned long long m = __ballot(i < mlim && s.cw[i + 1] > s.cw[i]);
       if (m) m0 = i0 + __builtin_ctzll(m);
     }
     if (m0 < 0 && cap <= setcap / 2) {
       need = cap;                           // flat up to the cap: every node is kept until the cap
+      tight = true;
+      tau = top - drop_fixed(need);
     } else if (m0 < 0 || m0 >= setcap / 2) {
       if (lane == 0) n_star_out[b] = -1;    // flat for longer than the set holds: the serial kernel's case
       return;
     } else {
       need = m0 + 1;
       const int m = m0 + 32 < cap ? m0 + 32 : cap;
-      tau = log(2.0 * (cost(m0 + 1) - cost(m0)) / cost(m)) - 0.5;
+      cc.ensure(m + 1, lane);
+      tau = log(2.0 * (s.cw[m0 + 1] - s.cw[m0]) / s.cw[m]) - 0.5;
+      if (need > 1) {
+        tau -= kDropFlat;
+        tight = true;
+      }
     }
-  } else if (fixed) {
-    need = cap;
   }
   tau = fmin(tau, top);
 
-  double lo = -INFINITY, hi = INFINITY;
   int n = 0, ns = 0;
   double phi = 0.0, theta = theta0;
   bool all_kept = false;                    // every node of T(tau) is kept (no flags written)
   bool done = cap == 0;
-  for (int attempt = 0; attempt < kMaxAttempts && !done; ++attempt) {
+  bool failed = false;
+  for (int attempt = 0; attempt < kMaxAttempts && !done && !failed; ++attempt) {
+    // what a raise keeps at most: a little above need when need is what the tree keeps
+    // before any stop test, else room for a stop past need
+    int keep_hi;
+    if (tight) {
+      keep_hi = need + need / 4 + 32;
+    } else {
+      const int half = setcap / 2, mid = (need + setcap) / 2;
+      keep_hi = need <= 1 || half > mid ? half : mid;
+    }
+    if (keep_hi > setcap) keep_hi = setcap;
     // ---- 1. T(tau), level by level
-    bool over = false, cut = false;
+    bool cut = false;
     {
       const bool live = lane < K;
       double x = 0.0, l1 = 0.0;
@@ -400,65 +630,68 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       cut = ns < K;
     }
     int la = 0, lb = ns;                    // the current level is [la, lb)
-    for (int d = 1; d < L && la < lb && !over; ++d) {
-      __syncthreads();
+    int raises = 0;
+    for (int d = 1; d < L && la < lb;) {
       const double Ad = rl_d(Areg, d + 1);
+      const double tlv = lane < K ? (double)s.tl[d * K + lane] : 0.0;   // lane r: rank r at depth d + 1
       int nb = lb;
+      bool over = false;
       for (int p0 = la; p0 < lb; p0 += kW) {
         const int p = p0 + lane;
         const bool live = p < lb;
         const double2 pv = s.sl[live ? p : la];
-        int c = 0;
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          c += (int)(r < K) & (int)((pv.y + (double)s.tl[d * K + (r < K ? r : 0)]) - Ad >= tau);
-        c = live ? c : 0;
+        int c = 0, rmax = 0;
+        for (; rmax < K; ++rmax) {
+          const bool q = live && (pv.y + rl_d(tlv, rmax)) - Ad >= tau;
+          if (__ballot(q) == 0) break;
+          c += q ? 1 : 0;
+        }
         const int incl = wave_incl_scan(c);
         const int tot = __builtin_amdgcn_readlane(incl, kW - 1);
         const int off = incl - c;
         if (live && c < K) cut = true;
         if (nb + tot > setcap) { over = true; break; }
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
+        for (int r = 0; r < rmax; ++r) {
+          const double t = rl_d(tlv, r);
           if (r < c) {
             const int i = nb + off + r;
-            const double l = pv.y + (double)s.tl[d * K + r];
+            const double l = pv.y + t;
             s.sl[i] = make_double2(pmin(l - Ad, pv.x), l);
             s.meta[i] = pack(p, r, d + 1);
           }
         }
         nb += tot;
       }
+      if (over) {
+        const double t2 = ++raises > kMaxRaises ? NAN : raise_tau(s, la, lb, K, Ad, tlv, tau, top, keep_hi, need, lane);
+        if (!(t2 > tau)) { failed = true; break; }
+        tau = t2;
+        cut = true;                          // nodes were dropped: the tree continues below tau
+        continue;                            // build depth d + 1 again
+      }
       la = lb;
       lb = nb;
+      ++d;
     }
+    if (failed) break;
     cut = __ballot(cut) != 0;
-    if (over) {
-      lo = tau;
-      tau = hi < INFINITY ? 0.5 * (tau + hi) : tau + 1.5;
-      tau = fmin(tau, top);
-      if (!(lo < tau)) break;               // the set cannot shrink further
-      continue;
-    }
     ns = lb;
     if (cut && ns < need && ns < cap) {     // too few nodes to hold the stop: lower tau without selecting
-      hi = tau;
-      const double step = fmin(fmax(log(1.5 * (double)need / (double)(ns > 0 ? ns : 1)), 0.5), 4.0);
-      tau = lower_tau(tau, tau - step, lo);
+      tau -= fmax(log(4.0 * (double)need / (double)(ns > 0 ? ns : 1)), 1.0);
       continue;
     }
-    __syncthreads();
 
     // ---- 2. where the stop falls
+    cc.ensure((ns < cap ? ns : cap) + 2, lane);   // C(m), C(m + 1) at every position, and C(ns + 1)
     Stop st;
     const unsigned seed = 0x9E3779B9u ^ (unsigned)b ^ ((unsigned)attempt << 16);
-    if (ns <= kW) st = stop_small(s, ns, cap, fixed, cost, lane);
-    else if (ns <= 2 * kW) st = stop_large<2>(s, ns, cap, fixed, cost, lane, seed);
-    else if (ns <= 4 * kW) st = stop_large<4>(s, ns, cap, fixed, cost, lane, seed);
-    else if (ns <= kSmall) st = stop_large<8>(s, ns, cap, fixed, cost, lane, seed);
-    else st = stop_lds(s, ns, cap, fixed, cost, lane, seed);
+    if (ns <= kW) st = stop_small(s, ns, cap, fixed, lane);
+    else if (ns <= 2 * kW) st = stop_reg<2>(s, ns, cap, fixed, lane, seed);
+    else if (ns <= 4 * kW) st = stop_reg<4>(s, ns, cap, fixed, lane, seed);
+    else if (ns <= kSmall) st = stop_reg<8>(s, ns, cap, fixed, lane, seed);
+    else st = stop_lds(s, ns, cap, fixed, lane, seed);
 
-    if (st.n < ns) {                        // the stop (or the cap) falls inside T(tau)
+    if (!st.all) {                          // the stop (or the cap) falls inside T(tau)
       n = st.n;
       phi = st.phi;
       all_kept = false;
@@ -469,17 +702,19 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       all_kept = true;
       done = true;
     } else {                                // every node kept: the stop lies below tau
-      hi = tau;
+      need = ns + 1;                        // and the tree holds more nodes than this set
+      tight = false;
+      if (need > setcap) { failed = true; break; }
       // the next pop is kept only while delta > (1 + Phi) c_{n+1} / C(n) (Lemma 1), a bound that
       // does not fall as n grows under a convex cost: aim a little below it
       double target = tau - 1.5;
       if (!fixed) {
-        const double c1 = cost(ns + 1) - cost(ns);
-        if (c1 > 0.0) target = fmin(tau - 0.25, log((1.0 + st.phi) * c1 / cost(ns)) - 1.0);
+        const double c1 = s.cw[ns + 1] - s.cw[ns];
+        if (c1 > 0.0) target = fmin(tau - 0.25, log((1.0 + st.phi) * c1 / s.cw[ns]) - 1.0);
       }
-      tau = lower_tau(tau, target, lo);
+      tau = target;
     }
-    if (done) theta = n == 0 ? theta0 : (1.0 + phi) / cost(n);
+    if (done) theta = n == 0 ? theta0 : (1.0 + phi) / rc(n);
   }
   if (!done) {
     if (lane == 0) n_star_out[b] = -1;      // left to the serial kernel
@@ -493,17 +728,14 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   if (n == 0) return;
 
   // ---- breadth-first positions: kept nodes before this one in generation order
-  __syncthreads();                          // the kept flags written by the selection
   int base = 0;
   for (int i0 = 0; i0 < ns; i0 += kW) {
     const int i = i0 + lane;
     const bool kept = i < ns && (all_kept || s.pos[i] != 0);
     const unsigned long long m = __ballot(kept);
-    const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
-    if (i < ns) s.pos[i] = kept ? (int16_t)(base + below) : (int16_t)-1;
+    if (i < ns) s.pos[i] = kept ? (int16_t)(base + lane_below(m)) : (int16_t)-1;
     base += __popcll(m);
   }
-  __syncthreads();
   const int64_t ob = (int64_t)b * cap;
   for (int i = lane; i < ns; i += kW) {
     const int o = s.pos[i];

@@ -144,6 +144,36 @@ def test_expand_paths_agree(name, kw, monkeypatch):
     _paths_agree(outs)
 
 
+@pytest.mark.parametrize("kw", [
+    dict(cost="c4", cap=400),                # convex cost
+    dict(cost="c3", cap=400),                # flat start: 65 nodes kept before any cost
+    dict(cost="tiny", cap=600),              # almost flat: trees of hundreds of nodes
+    dict(cost="c4", cap=150, fixed=True),    # fixed budget
+])
+def test_expand_paths_agree_on_ties(kw, monkeypatch):
+    """Logits on a 0.5 grid, one boosted token per position: many nodes tie on sigma (and on
+    Lambda), so the batched kernel's sigma-order selection, its cut tie groups and its in-place
+    threshold raises all run; its trees must equal the serial kernel's."""
+    import torch
+    cfg = synth.get_config("c4").replace(V=1500, B=96, L=8, K=16, **kw)
+    rng = np.random.default_rng(11)
+    x = np.round(rng.standard_normal((cfg.B, cfg.L, cfg.V)) * 2.0) / 2.0
+    peak = rng.integers(0, cfg.V, size=(cfg.B, cfg.L))
+    x[np.arange(cfg.B)[:, None], np.arange(cfg.L)[None, :], peak] += rng.choice([0.0, 3.0, 6.0], size=(cfg.B, cfg.L))
+    lg = torch_logits(cfg, x.astype(np.float32))
+    outs = {}
+    for mode in ("auto", "serial"):
+        if mode == "serial":
+            monkeypatch.setenv("CADDTREE_EXPAND", "serial")
+        else:
+            monkeypatch.delenv("CADDTREE_EXPAND", raising=False)
+        plan = make_plan(cfg)
+        outs[mode] = host(run_build(plan, lg))
+    n = outs["auto"]["n_star"]
+    say(f"[paths ties] {kw} n* mean {n.mean():.1f} min {n.min()} max {n.max()}")
+    _paths_agree(outs)
+
+
 def _paths_agree(outs):
     """The two expansion kernels give the same trees; Phi (and theta from it) may differ by the
     rounding of the summation order, far below the fp32 output precision."""
