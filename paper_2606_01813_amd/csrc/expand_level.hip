@@ -27,12 +27,13 @@
 //       path probabilities are scattered into that order, a prefix sum gives
 //       Phi before every position m, and m is kept iff
 //       (1 + Phi_m + delta_m) / C(m + 1) > (1 + Phi_m) / C(m) and m < cap;
+//     * 65 to 128 nodes: the same, with every node ranked by one counting pass;
 //     * larger sets: under a convex cost theta rises and then falls along the
-//       pop order (Thm. 1), so "the first position holding sigma value v is
-//       kept" holds for the large values and fails for the small ones, and a
-//       bisection over the sigma values finds the last value that passes; the
-//       stop then lies inside its tie group, whose positions are tested in
-//       parallel;
+//       pop order (Thm. 1), so the stop test fails from n* on.  A 64-bin
+//       histogram of sigma gives the position of each bin's first node and
+//       Phi before it, the test runs at every bin's first node at once, and
+//       the bin that holds the stop is ranked node by node (or split again by
+//       a histogram of its own range when it holds more than 64 nodes);
 //     with a fixed budget m is kept iff m < cap;
 //  3. if every node of T(tau) is kept and the tree continues below tau, lower
 //     tau and start again; likewise when T(tau) holds fewer nodes than every
@@ -107,13 +108,16 @@ struct Lds {
   uint32_t* meta;   // [S]   packed word (parent, rank, depth)
   double* dl;       // [S]   path probability (sets above kSmall), or in sigma order (small sets)
   int16_t* pos;     // [S]   new index (raise), kept flag, then breadth-first position
-  int* hist;        // [kBins]
+  unsigned long long* hsum;   // [kBins] fixed-point delta sums (selection)
+  unsigned long long* hmax;   // [kBins] largest sigma, as an ordered key (selection)
+  unsigned long long* hmin;   // [kBins] smallest sigma, as an ordered key (selection)
+  int* hist;                  // [kBins] node counts (raise, selection)
 };
 
 // LDS of a round for a set of S nodes
 __host__ __device__ constexpr size_t level_lds_bytes(size_t LK, size_t S) {
   return a16(a16(a16(a16(a16(a16(a16(a16(4 * LK) + 4 * LK) + 8 * (S + 2)) + 16 * S) + 4 * S) + 8 * S) + 2 * S) +
-             4 * (size_t)kBins);
+             32 * (size_t)kBins);
 }
 static_assert(level_lds_bytes((size_t)CADDTREE_MAX_L * CADDTREE_MAX_K, kMaxSet) <= 160 * 1024,
               "the largest set must fit in the LDS of one CU");
@@ -128,7 +132,10 @@ __device__ Lds carve(unsigned char* smem, size_t LK, size_t S) {
   s.meta = reinterpret_cast<uint32_t*>(smem + off); off = a16(off + 4 * S);
   s.dl = reinterpret_cast<double*>(smem + off);     off = a16(off + 8 * S);
   s.pos = reinterpret_cast<int16_t*>(smem + off);   off = a16(off + 2 * S);
-  s.hist = reinterpret_cast<int*>(smem + off);
+  s.hsum = reinterpret_cast<unsigned long long*>(smem + off);
+  s.hmax = s.hsum + kBins;
+  s.hmin = s.hmax + kBins;
+  s.hist = reinterpret_cast<int*>(s.hmin + kBins);
   return s;
 }
 
@@ -264,79 +271,77 @@ __device__ __forceinline__ int group_stop(int mA, double phA, double dA, int tA,
   return tA;
 }
 
-// larger sets held in registers: P sigma values per lane, node e = j * 64 + lane
+// Sets of 65 .. 64 P nodes held in registers (node e = j * 64 + lane): every node's position in
+// sigma order (ties by index) by one counting pass over the set, read from LDS as a broadcast;
+// the path probabilities are scattered into that order, and the stop test runs at every
+// position in parallel, 64 positions at a time, with Phi carried across them.
 template <int P>
-__device__ Stop stop_reg(const Lds& s, int ns, int cap, int fixed, int lane, unsigned seed) {
-  double sg[P], dl[P];
+__device__ Stop stop_rank(const Lds& s, int ns, int cap, int fixed, int lane) {
+  double sg[P];
+  int r[P];
 #pragma unroll
   for (int j = 0; j < P; ++j) {
     const int e = j * kW + lane;
     sg[j] = e < ns ? s.sl[e].x : -INFINITY;
-    dl[j] = e < ns ? exp(sg[j]) : 0.0;
+    r[j] = 0;
   }
-  // bisection over the sigma values: vA is the smallest value seen whose first position is
-  // kept, vB the largest value seen whose first position is not
-  bool hasA = false, hasB = false;
-  double vA = 0.0, vB = 0.0, dA = 0.0, phA = 0.0;
-  int mA = 0;
-  unsigned rng = seed;
-  for (;;) {
-    unsigned long long cm[P];
-    int total = 0;
+  int o = 0;
+  for (; o + 4 <= ns; o += 4) {
+    double so[4];
 #pragma unroll
-    for (int j = 0; j < P; ++j) {
-      const bool c = j * kW + lane < ns && (!hasA || sg[j] < vA) && (!hasB || sg[j] > vB);
-      cm[j] = __ballot(c);
-      total += __popcll(cm[j]);
-    }
-    if (total == 0) break;
-    rng = rng * 1664525u + 1013904223u;
-    int k = (int)((rng >> 8) % (unsigned)total);
-    int pj = 0;
-    unsigned long long mk = cm[0];
+    for (int u = 0; u < 4; ++u) so[u] = s.sl[o + u].x;
 #pragma unroll
-    for (int j = 0; j + 1 < P; ++j) {
-      const int c = __popcll(cm[j]);
-      if (pj == j && k >= c) { k -= c; pj = j + 1; mk = cm[j + 1]; }
-    }
-    const int pl = __builtin_ctzll(__ballot(((mk >> lane) & 1ull) && lane_below(mk) == k));
-    double v = 0.0, pd = 0.0;
+    for (int u = 0; u < 4; ++u)
 #pragma unroll
-    for (int j = 0; j < P; ++j)
-      if (j == pj) { v = rl_d(sg[j], pl); pd = rl_d(dl[j], pl); }
-    int cnt = 0;
-    double part = 0.0;
-#pragma unroll
-    for (int j = 0; j < P; ++j) {
-      const bool bf = sg[j] > v;
-      cnt += __popcll(__ballot(bf));
-      part += bf ? dl[j] : 0.0;
-    }
-    const double ph = rl_d(wave_incl_scan(part), kW - 1);
-    if (kept_at(cnt, ph, pd, cap, fixed, s.cw)) { hasA = true; vA = v; dA = pd; mA = cnt; phA = ph; }
-    else { hasB = true; vB = v; }
+      for (int j = 0; j < P; ++j)
+        r[j] += (int)(so[u] > sg[j]) | ((int)(so[u] == sg[j]) & (int)(o + u < j * kW + lane));
   }
-  if (!hasA) {                                // not even the first position is kept
+  for (; o < ns; ++o) {
+    const double so = s.sl[o].x;
 #pragma unroll
-    for (int j = 0; j < P; ++j)
-      if (j * kW + lane < ns) s.pos[j * kW + lane] = 0;
-    return Stop{0, 0.0, false};
+    for (int j = 0; j < P; ++j) r[j] += (int)(so > sg[j]) | ((int)(so == sg[j]) & (int)(o < j * kW + lane));
   }
-  int tA = 0;
 #pragma unroll
-  for (int j = 0; j < P; ++j) tA += __popcll(__ballot(j * kW + lane < ns && sg[j] == vA));
-  const int ks = group_stop(mA, phA, dA, tA, cap, fixed, s.cw, lane);
-  const int n = mA + ks;
-  const double phi = phA + (double)ks * dA;
-  if (n == ns) return Stop{ns, phi, true};
-  if (ks < tA) {
-    cut_group_flags<P>(s, ns, sg, vA, mA, n, lane);
+  for (int j = 0; j < P; ++j)
+    if (j * kW + lane < ns) s.dl[r[j]] = exp(sg[j]);
+  double carry = 0.0;                         // Phi before the current 64 positions
+  int stop = ns;
+  double phi = 0.0;
+  for (int p0 = 0; p0 < ns; p0 += kW) {
+    const int p = p0 + lane;
+    const bool live = p < ns;
+    const double d = live ? s.dl[p] : 0.0;
+    const double incl = wave_incl_scan(d);
+    const double pe = carry + wave_shr1(incl);  // Phi before position p
+    const bool keep = live && kept_at(p, pe, d, cap, fixed, s.cw);
+    const unsigned long long fm = __ballot(live && !keep);
+    if (fm) {
+      const int l = __builtin_ctzll(fm);
+      stop = p0 + l;
+      phi = rl_d(pe, l);
+      break;
+    }
+    carry += rl_d(incl, kW - 1);
+  }
+  if (stop == ns) return Stop{ns, carry, true};
+  // the tie group at the stop position
+  double v = 0.0;
+#pragma unroll
+  for (int j = 0; j < P; ++j) {
+    const unsigned long long m = __ballot(j * kW + lane < ns && r[j] == stop);
+    if (m) v = rl_d(sg[j], __builtin_ctzll(m));
+  }
+  int g0 = 0;
+#pragma unroll
+  for (int j = 0; j < P; ++j) g0 += __popcll(__ballot(sg[j] > v));
+  if (g0 < stop) {
+    cut_group_flags<P>(s, ns, sg, v, g0, stop, lane);
   } else {
 #pragma unroll
     for (int j = 0; j < P; ++j)
-      if (j * kW + lane < ns) s.pos[j * kW + lane] = sg[j] >= vA ? 1 : 0;
+      if (j * kW + lane < ns) s.pos[j * kW + lane] = sg[j] > v ? 1 : 0;
   }
-  return Stop{n, phi, false};
+  return Stop{stop, phi, false};
 }
 
 // sets above kSmall nodes: the same bisection with the values read from LDS at every step
@@ -426,6 +431,155 @@ __device__ Stop stop_lds(const Lds& s, int ns, int cap, int fixed, int lane, uns
     if (live) s.pos[e] = mA + rt < n ? 1 : 0;
   }
   return Stop{n, phi, false};
+}
+
+// order-preserving 64-bit key of a double, and back
+__device__ __forceinline__ unsigned long long dkey(double x) {
+  const unsigned long long b = (unsigned long long)__double_as_longlong(x);
+  return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
+}
+__device__ __forceinline__ double dkey_inv(unsigned long long k) {
+  const unsigned long long b = (k >> 63) ? (k & 0x7FFFFFFFFFFFFFFFull) : ~k;
+  return __longlong_as_double((long long)b);
+}
+constexpr double kFix = 0x1p50;   // fixed-point scale of delta in the bin sums (at most 4096 * 2^50 < 2^63)
+
+// Sets above 128 nodes, in LDS.  A 64-bin histogram over the range of sigma gives, per bin,
+// the node count, the largest and smallest sigma and the sum of delta in fixed point
+// (integer atomics, so the sums do not depend on the order of the additions; their error,
+// below ns * 2^-50, is far under the stop margins the inputs keep).  Bins are monotone in
+// sigma, so the first node of every bin sits at a known position with a known Phi before
+// it, and the stop test at the first node of every bin runs in parallel.  The stop lies in
+// the last bin whose first node passes.  A bin of at most 64 nodes is ranked by sigma (ties
+// by index) and tested one node per lane; a larger one is split by a histogram of its own
+// range, up to kLevels deep.  s.pos marks each node kept (1), not kept (0) or still open (2).
+// A bin of more than 64 equal values, or deeper nesting, falls back to the bisection.
+constexpr int kLevels = 4;
+
+__device__ Stop stop_hist(const Lds& s, int ns, int cap, int fixed, double lo, double hi, int lane, unsigned seed) {
+  int base_m = 0;                         // position of the open range's first node
+  double base_p = 0.0;                    // Phi before it
+  for (int level = 0; level < kLevels; ++level) {
+    if (!(hi > lo)) break;
+    const double scale = (double)kBins / (hi - lo);
+    auto bin = [&](double v) -> int {
+      const int b = (int)((v - lo) * scale);
+      return b < 0 ? 0 : (b < kBins - 1 ? b : kBins - 1);
+    };
+    auto open = [&](int e) -> bool { return level == 0 || s.pos[e] == 2; };
+    s.hist[lane] = 0;
+    s.hmax[lane] = 0ull;
+    s.hmin[lane] = ~0ull;
+    s.hsum[lane] = 0ull;
+    for (int e0 = 0; e0 < ns; e0 += kW) {
+      const int e = e0 + lane;
+      if (e < ns && open(e)) {
+        const double v = s.sl[e].x;
+        double d;
+        if (level == 0) {
+          d = exp(v);
+          s.dl[e] = d;
+        } else {
+          d = s.dl[e];
+        }
+        const int b = bin(v);
+        atomicAdd(&s.hist[b], 1);
+        atomicMax(&s.hmax[b], dkey(v));
+        atomicMin(&s.hmin[b], dkey(v));
+        atomicAdd(&s.hsum[b], (unsigned long long)(d * kFix));
+      }
+    }
+    // lane b holds bin b; in reversed lane order the prefix sums run from the top bin down
+    const int cnt = s.hist[lane];
+    const double fs = (double)s.hsum[lane] / kFix;
+    const double vmax = cnt ? dkey_inv(s.hmax[lane]) : 0.0;
+    const double vmin = cnt ? dkey_inv(s.hmin[lane]) : 0.0;
+    const int rl = kW - 1 - lane;
+    const int cr = __shfl(cnt, rl);
+    const double fr = __shfl(fs, rl);
+    const int ce = wave_incl_scan(cr) - cr;
+    const double fe = wave_shr1(wave_incl_scan(fr));
+    const int mb = base_m + __shfl(ce, rl);     // position of bin `lane`'s first node
+    const double pb = base_p + __shfl(fe, rl);  // Phi before it
+    const bool keep_b = cnt == 0 || kept_at(mb, pb, exp(vmax), cap, fixed, s.cw);
+    const unsigned long long fails = __ballot(!keep_b);
+    const unsigned long long full = __ballot(cnt > 0);
+    const unsigned long long above = fails ? full & ~((2ull << (63 - __builtin_clzll(fails))) - 1ull) : full;
+    if (above == 0) {                     // the open range's first node is not kept (level 0 only)
+      for (int e = lane; e < ns; e += kW)
+        if (open(e)) s.pos[e] = 0;
+      return Stop{base_m, base_p, false};
+    }
+    const int bk = __builtin_ctzll(above);      // the stop lies in this bin or right after it
+    const int t = __builtin_amdgcn_readlane(cnt, bk);
+    const int mk = __builtin_amdgcn_readlane(mb, bk);
+    const double pk = rl_d(pb, bk);
+    for (int e = lane; e < ns; e += kW)
+      if (open(e)) {
+        const int b = bin(s.sl[e].x);
+        s.pos[e] = b > bk ? 1 : (b < bk ? 0 : 2);
+      }
+    if (t > kW) {                         // split the bin by a histogram of its own range
+      lo = rl_d(vmin, bk);
+      hi = rl_d(vmax, bk);
+      base_m = mk;
+      base_p = pk;
+      continue;
+    }
+    // the bin's nodes, one per lane, in generation order
+    int* mem = s.hist;                    // the counts are in registers now
+    {
+      int nb = 0;
+      for (int e0 = 0; e0 < ns; e0 += kW) {
+        const int e = e0 + lane;
+        const bool g = e < ns && s.pos[e < ns ? e : 0] == 2;
+        const unsigned long long gm = __ballot(g);
+        if (g) mem[nb + lane_below(gm)] = e;
+        nb += __popcll(gm);
+      }
+    }
+    const bool live = lane < t;
+    const int me = mem[live ? lane : 0];
+    const double sg = live ? s.sl[me].x : -INFINITY;
+    int r = 0;
+    for (int o = 0; o < t; ++o) {
+      const double so = rl_d(sg, o);
+      r += (int)(so > sg) | ((int)(so == sg) & (int)(o < lane));
+    }
+    double* ds = reinterpret_cast<double*>(s.hsum);   // delta of the bin's nodes in sigma order
+    if (live) ds[r] = s.dl[me];
+    const double d = live ? ds[lane] : 0.0;
+    const double incl = wave_incl_scan(d);
+    const double pe = pk + wave_shr1(incl);           // Phi before position mk + lane
+    const bool keep = live && kept_at(mk + lane, pe, d, cap, fixed, s.cw);
+    const unsigned long long fm = __ballot(live && !keep);
+    const int ks = fm ? __builtin_ctzll(fm) : t;
+    const int n = mk + ks;
+    const double phi = fm ? rl_d(pe, ks) : pk + rl_d(incl, kW - 1);
+    if (n == ns) return Stop{ns, phi, true};
+    int kept = 1;
+    if (ks < t) {
+      const double v = rl_d(sg, __builtin_ctzll(__ballot(live && r == ks)));   // sigma at the stop
+      const int g0 = __popcll(__ballot(live && sg > v));
+      kept = r < ks;
+      if (g0 < ks) {                      // the stop cuts a tie group: its full pop order decides
+        const double lam = live ? s.sl[me].y : 0.0;
+        const uint32_t mm = live ? s.meta[me] : 0u;
+        int rt = 0;
+        for (int o = 0; o < t; ++o) {
+          const double so = rl_d(sg, o);
+          if (so == v)
+            rt += (live && sg == v &&
+                   pops_before(v, rl_d(lam, o), rl_u(mm, o), __builtin_amdgcn_readlane(me, o), v, lam, mm, me))
+                      ? 1 : 0;
+        }
+        kept = sg > v || (sg == v && g0 + rt < ks);
+      }
+    }
+    if (live) s.pos[me] = kept ? 1 : 0;
+    return Stop{n, phi, false};
+  }
+  return stop_lds(s, ns, cap, fixed, lane, seed);
 }
 
 // Raise tau in place at depth d.  Depths 1 .. d are s[0, lb) (depth d at [la, lb)); the
@@ -686,10 +840,8 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
     Stop st;
     const unsigned seed = 0x9E3779B9u ^ (unsigned)b ^ ((unsigned)attempt << 16);
     if (ns <= kW) st = stop_small(s, ns, cap, fixed, lane);
-    else if (ns <= 2 * kW) st = stop_reg<2>(s, ns, cap, fixed, lane, seed);
-    else if (ns <= 4 * kW) st = stop_reg<4>(s, ns, cap, fixed, lane, seed);
-    else if (ns <= kSmall) st = stop_reg<8>(s, ns, cap, fixed, lane, seed);
-    else st = stop_lds(s, ns, cap, fixed, lane, seed);
+    else if (ns <= 2 * kW) st = stop_rank<2>(s, ns, cap, fixed, lane);
+    else st = stop_hist(s, ns, cap, fixed, tau, top, lane, seed);
 
     if (!st.all) {                          // the stop (or the cap) falls inside T(tau)
       n = st.n;
