@@ -25,6 +25,7 @@ struct caddtree_plan {
   double* d_t_verify;   // device copy, n_ctx x (cap + 1) values
   int64_t* d_ctx_grid;  // device copy of the grid (n_ctx >= 2), else NULL
   bool use_level;       // the batched expansion applies (see plan_create)
+  bool flat_cost;       // every cost table holds one value up to the cap
   int level_set_cap;    // its threshold-set capacity
   int device;
   int k1_waves;         // 0 = automatic
@@ -158,6 +159,7 @@ caddtree_status_t run_expand(const caddtree_plan* p, const int32_t* ids, const f
   a.use_level = p->use_level;
   a.level_set_cap = p->level_set_cap;
   a.fixed_budget = (p->flags & CADDTREE_FIXED_BUDGET) != 0;
+  a.flat_cost = p->flat_cost;
   hipError_t e = caddtree::launch_expand(a, stream);
   if (e != hipSuccess) return hip_fail(e, "expand launch");
   return CADDTREE_OK;
@@ -240,6 +242,7 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
   const int cap = cfg->budget_cap;
   int flat_start = 0;     // the most leading zero marginal costs over the tables
   bool convex = true;
+  bool flat_cost = true;  // every table holds one value (bit for bit) up to the cap
   for (int j = 0; j < J; ++j) {
     const double* tv = cfg->t_verify_host + (size_t)j * (size_t)(cap + 1);
     double scale = 0.0;
@@ -262,6 +265,7 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
     int m0 = 0;
     while (m0 < cap && !(tv[m0 + 1] > tv[m0])) ++m0;
     flat_start = std::max(flat_start, m0);
+    for (int n = 1; n <= cap && flat_cost; ++n) flat_cost = tv[n] == tv[0];
   }
 
   caddtree_plan* p = new (std::nothrow) caddtree_plan();
@@ -282,11 +286,14 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
   // that holds at least the nodes every tree keeps: the budget with a fixed
   // budget or a cost flat up to the cap, else the nodes before the first
   // positive marginal cost (the most over the tables).  The set is sized to
-  // twice that, 512 .. 4096 nodes.
+  // twice that, 512 .. 4096 nodes.  Fixed budgets and flat costs need no cost
+  // table in LDS, which leaves room for 5120 nodes (trees of up to 4096).
   const bool fixed = (cfg->flags & CADDTREE_FIXED_BUDGET) != 0;
+  const bool lean = fixed || flat_cost;
   const int need = (fixed || flat_start >= cap) ? cap : flat_start + 1;
-  p->use_level = cap >= 1 && (fixed || convex) && need <= caddtree::expand_level_max_need();
-  p->level_set_cap = caddtree::expand_level_set_cap(need);
+  p->flat_cost = flat_cost;
+  p->use_level = cap >= 1 && (fixed || convex) && need <= caddtree::expand_level_max_need(lean);
+  p->level_set_cap = caddtree::expand_level_set_cap(need, lean);
   if (const char* env = std::getenv("CADDTREE_EXPAND")) {
     if (std::strcmp(env, "serial") == 0) p->use_level = false;
   }

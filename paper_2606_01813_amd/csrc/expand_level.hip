@@ -72,6 +72,7 @@ using namespace xp;
 constexpr int kW = 64;
 constexpr int kSmall = 512;           // sets up to this size are selected in registers
 constexpr int kMaxSet = 4096;         // the largest set the LDS layout holds
+constexpr int kMaxLeanSet = 5120;     // the same without the cost table (fixed budgets, flat costs)
 constexpr int kMaxAttempts = 12;
 constexpr int kBins = kW;             // histogram bins of the in-place raise (one per lane)
 constexpr int kRefine = 4;            // histogram passes per raise
@@ -115,19 +116,25 @@ struct Lds {
 };
 
 // LDS of a round for a set of S nodes
-__host__ __device__ constexpr size_t level_lds_bytes(size_t LK, size_t S) {
-  return a16(a16(a16(a16(a16(a16(a16(a16(4 * LK) + 4 * LK) + 8 * (S + 2)) + 16 * S) + 4 * S) + 8 * S) + 2 * S) +
+// (lean: no cost table, for fixed budgets and costs flat up to the cap)
+__host__ __device__ constexpr size_t cost_entries(size_t S, bool lean) { return lean ? 0 : S + 2; }
+__host__ __device__ constexpr size_t level_lds_bytes(size_t LK, size_t S, bool lean) {
+  return a16(a16(a16(a16(a16(a16(a16(a16(4 * LK) + 4 * LK) + 8 * cost_entries(S, lean)) + 16 * S) + 4 * S) + 8 * S) +
+                 2 * S) +
              32 * (size_t)kBins);
 }
-static_assert(level_lds_bytes((size_t)CADDTREE_MAX_L * CADDTREE_MAX_K, kMaxSet) <= 160 * 1024,
-              "the largest set must fit in the LDS of one CU");
+constexpr size_t kMaxLds = level_lds_bytes((size_t)CADDTREE_MAX_L * CADDTREE_MAX_K, kMaxSet, false) >
+                                   level_lds_bytes((size_t)CADDTREE_MAX_L * CADDTREE_MAX_K, kMaxLeanSet, true)
+                               ? level_lds_bytes((size_t)CADDTREE_MAX_L * CADDTREE_MAX_K, kMaxSet, false)
+                               : level_lds_bytes((size_t)CADDTREE_MAX_L * CADDTREE_MAX_K, kMaxLeanSet, true);
+static_assert(kMaxLds <= 160 * 1024, "the largest set must fit in the LDS of one CU");
 
-__device__ Lds carve(unsigned char* smem, size_t LK, size_t S) {
+__device__ Lds carve(unsigned char* smem, size_t LK, size_t S, bool lean) {
   Lds s;
   size_t off = 0;
   s.tl = reinterpret_cast<float*>(smem + off);      off = a16(off + 4 * LK);
   s.tid = reinterpret_cast<int32_t*>(smem + off);   off = a16(off + 4 * LK);
-  s.cw = reinterpret_cast<double*>(smem + off);     off = a16(off + 8 * (S + 2));
+  s.cw = reinterpret_cast<double*>(smem + off);     off = a16(off + 8 * cost_entries(S, lean));
   s.sl = reinterpret_cast<double2*>(smem + off);    off = a16(off + 16 * S);
   s.meta = reinterpret_cast<uint32_t*>(smem + off); off = a16(off + 4 * S);
   s.dl = reinterpret_cast<double*>(smem + off);     off = a16(off + 8 * S);
@@ -169,11 +176,22 @@ struct CostCache {
   }
 };
 
+// The stop test of a round: a fixed budget keeps every position below the cap; a cost flat up
+// to the cap has C(m) = C(0) at every position (no table); else C(m) comes from the LDS table.
+struct StopTest {
+  int cap;
+  int fixed;
+  int flat;
+  double c0;         // C(0)
+  const double* cw;  // C(0 ..), costs that are neither fixed budgets nor flat
+};
+
 // position m of the pop order is kept, with Phi before it and delta at it
-__device__ __forceinline__ bool kept_at(int m, double phi, double delta, int cap, int fixed, const double* cw) {
-  if (m >= cap) return false;
-  if (fixed) return true;
-  return (1.0 + phi + delta) / cw[m + 1] > (1.0 + phi) / cw[m];
+__device__ __forceinline__ bool kept_at(int m, double phi, double delta, const StopTest& t) {
+  if (m >= t.cap) return false;
+  if (t.fixed) return true;
+  if (t.flat) return (1.0 + phi + delta) / t.c0 > (1.0 + phi) / t.c0;
+  return (1.0 + phi + delta) / t.cw[m + 1] > (1.0 + phi) / t.cw[m];
 }
 
 struct Stop {
@@ -221,7 +239,7 @@ __device__ void cut_group_flags(const Lds& s, int ns, const double (&sg)[P], dou
 
 // up to 64 nodes: rank by sigma (ties by index), Phi by a prefix sum over those positions;
 // on a stop inside the set, the kept flags go to s.pos by generation index
-__device__ Stop stop_small(const Lds& s, int ns, int cap, int fixed, int lane) {
+__device__ Stop stop_small(const Lds& s, int ns, const StopTest& tst, int lane) {
   const bool live = lane < ns;
   double sg[1];
   sg[0] = live ? s.sl[lane].x : -INFINITY;
@@ -243,7 +261,7 @@ __device__ Stop stop_small(const Lds& s, int ns, int cap, int fixed, int lane) {
   const double d = live ? s.dl[lane] : 0.0;   // delta at position `lane`
   const double incl = wave_incl_scan(d);
   const double pe = wave_shr1(incl);          // Phi before position `lane`
-  const bool keep = live && kept_at(lane, pe, d, cap, fixed, s.cw);
+  const bool keep = live && kept_at(lane, pe, d, tst);
   const unsigned long long fm = __ballot(live && !keep);
   if (!fm) return Stop{ns, rl_d(incl, kW - 1), true};
   const int stop = __builtin_ctzll(fm);
@@ -260,11 +278,10 @@ __device__ Stop stop_small(const Lds& s, int ns, int cap, int fixed, int lane) {
 
 // The stop inside the tie group of value vA (first position mA, Phi before it phA, delta dA,
 // tA members): the offset of the first member position that is not kept, or tA.
-__device__ __forceinline__ int group_stop(int mA, double phA, double dA, int tA, int cap, int fixed,
-                                          const double* cw, int lane) {
+__device__ __forceinline__ int group_stop(int mA, double phA, double dA, int tA, const StopTest& tst, int lane) {
   for (int k0 = 1; k0 < tA; k0 += kW) {
     const int k = k0 + lane;
-    const bool bad = k < tA && !kept_at(mA + k, phA + (double)k * dA, dA, cap, fixed, cw);
+    const bool bad = k < tA && !kept_at(mA + k, phA + (double)k * dA, dA, tst);
     const unsigned long long bm = __ballot(bad);
     if (bm) return k0 + __builtin_ctzll(bm);
   }
@@ -276,7 +293,7 @@ __device__ __forceinline__ int group_stop(int mA, double phA, double dA, int tA,
 // the path probabilities are scattered into that order, and the stop test runs at every
 // position in parallel, 64 positions at a time, with Phi carried across them.
 template <int P>
-__device__ Stop stop_rank(const Lds& s, int ns, int cap, int fixed, int lane) {
+__device__ Stop stop_rank(const Lds& s, int ns, const StopTest& tst, int lane) {
   double sg[P];
   int r[P];
 #pragma unroll
@@ -313,7 +330,7 @@ __device__ Stop stop_rank(const Lds& s, int ns, int cap, int fixed, int lane) {
     const double d = live ? s.dl[p] : 0.0;
     const double incl = wave_incl_scan(d);
     const double pe = carry + wave_shr1(incl);  // Phi before position p
-    const bool keep = live && kept_at(p, pe, d, cap, fixed, s.cw);
+    const bool keep = live && kept_at(p, pe, d, tst);
     const unsigned long long fm = __ballot(live && !keep);
     if (fm) {
       const int l = __builtin_ctzll(fm);
@@ -345,7 +362,7 @@ __device__ Stop stop_rank(const Lds& s, int ns, int cap, int fixed, int lane) {
 }
 
 // sets above kSmall nodes: the same bisection with the values read from LDS at every step
-__device__ Stop stop_lds(const Lds& s, int ns, int cap, int fixed, int lane, unsigned seed) {
+__device__ Stop stop_lds(const Lds& s, int ns, const StopTest& tst, int lane, unsigned seed) {
   for (int e = lane; e < ns; e += kW) s.dl[e] = exp(s.sl[e].x);
   bool hasA = false, hasB = false;
   double vA = 0.0, vB = 0.0, dA = 0.0, phA = 0.0;
@@ -380,7 +397,7 @@ __device__ Stop stop_lds(const Lds& s, int ns, int cap, int fixed, int lane, uns
       part += bf ? s.dl[e] : 0.0;
     }
     const double ph = rl_d(wave_incl_scan(part), kW - 1);
-    if (kept_at(cnt, ph, pd, cap, fixed, s.cw)) { hasA = true; vA = v; dA = pd; mA = cnt; phA = ph; }
+    if (kept_at(cnt, ph, pd, tst)) { hasA = true; vA = v; dA = pd; mA = cnt; phA = ph; }
     else { hasB = true; vB = v; }
   }
   if (!hasA) {
@@ -392,7 +409,7 @@ __device__ Stop stop_lds(const Lds& s, int ns, int cap, int fixed, int lane, uns
     const int e = e0 + lane;
     tA += __popcll(__ballot(e < ns && s.sl[e < ns ? e : 0].x == vA));
   }
-  const int ks = group_stop(mA, phA, dA, tA, cap, fixed, s.cw, lane);
+  const int ks = group_stop(mA, phA, dA, tA, tst, lane);
   const int n = mA + ks;
   const double phi = phA + (double)ks * dA;
   if (n == ns) return Stop{ns, phi, true};
@@ -456,7 +473,7 @@ constexpr double kFix = 0x1p50;   // fixed-point scale of delta in the bin sums 
 // A bin of more than 64 equal values, or deeper nesting, falls back to the bisection.
 constexpr int kLevels = 4;
 
-__device__ Stop stop_hist(const Lds& s, int ns, int cap, int fixed, double lo, double hi, int lane, unsigned seed) {
+__device__ Stop stop_hist(const Lds& s, int ns, const StopTest& tst, double lo, double hi, int lane, unsigned seed) {
   int base_m = 0;                         // position of the open range's first node
   double base_p = 0.0;                    // Phi before it
   for (int level = 0; level < kLevels; ++level) {
@@ -501,7 +518,7 @@ __device__ Stop stop_hist(const Lds& s, int ns, int cap, int fixed, double lo, d
     const double fe = wave_shr1(wave_incl_scan(fr));
     const int mb = base_m + __shfl(ce, rl);     // position of bin `lane`'s first node
     const double pb = base_p + __shfl(fe, rl);  // Phi before it
-    const bool keep_b = cnt == 0 || kept_at(mb, pb, exp(vmax), cap, fixed, s.cw);
+    const bool keep_b = cnt == 0 || kept_at(mb, pb, exp(vmax), tst);
     const unsigned long long fails = __ballot(!keep_b);
     const unsigned long long full = __ballot(cnt > 0);
     const unsigned long long above = fails ? full & ~((2ull << (63 - __builtin_clzll(fails))) - 1ull) : full;
@@ -551,7 +568,7 @@ __device__ Stop stop_hist(const Lds& s, int ns, int cap, int fixed, double lo, d
     const double d = live ? ds[lane] : 0.0;
     const double incl = wave_incl_scan(d);
     const double pe = pk + wave_shr1(incl);           // Phi before position mk + lane
-    const bool keep = live && kept_at(mk + lane, pe, d, cap, fixed, s.cw);
+    const bool keep = live && kept_at(mk + lane, pe, d, tst);
     const unsigned long long fm = __ballot(live && !keep);
     const int ks = fm ? __builtin_ctzll(fm) : t;
     const int n = mk + ks;
@@ -579,7 +596,7 @@ __device__ Stop stop_hist(const Lds& s, int ns, int cap, int fixed, double lo, d
     if (live) s.pos[me] = kept ? 1 : 0;
     return Stop{n, phi, false};
   }
-  return stop_lds(s, ns, cap, fixed, lane, seed);
+  return stop_lds(s, ns, tst, lane, seed);
 }
 
 // Raise tau in place at depth d.  Depths 1 .. d are s[0, lb) (depth d at [la, lb)); the
@@ -670,7 +687,7 @@ __device__ double raise_tau(const Lds& s, int& la, int& lb, int K, double Ad, do
 __global__ void __launch_bounds__(kW)
 expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict__ topk_logit,
                     const double* __restrict__ lse, int L, int K, int cap, CostTables ct, int fixed,
-                    int setcap, int32_t* __restrict__ token_ids,
+                    int flat, int setcap, int32_t* __restrict__ token_ids,
                     int32_t* __restrict__ parent_out, int32_t* __restrict__ depth_out,
                     float* __restrict__ path_prob, int32_t* __restrict__ n_star_out,
                     float* __restrict__ phi_out, float* __restrict__ theta_out) {
@@ -678,7 +695,8 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   const int b = blockIdx.x;
   const int lane = threadIdx.x;
   const int LK = L * K;
-  const Lds s = carve(smem, (size_t)LK, (size_t)setcap);
+  const bool lean = fixed || flat;          // no cost table
+  const Lds s = carve(smem, (size_t)LK, (size_t)setcap, lean);
   const RoundCost rc = ct.round(b);
 
   // setup: the round's global loads are issued together, then stored to LDS.  Indices are
@@ -686,7 +704,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   // valid one), so neither loads nor stores sit behind branches.
   const double c0 = rc(0);
   const double lse_l = lse[(int64_t)b * L + (lane < L ? lane : L - 1)];
-  CostCache cc{rc, s.cw, cap, fixed ? 0 : (cap < setcap ? cap : setcap) + 2, 0};   // C(0 .. ncw - 1)
+  CostCache cc{rc, s.cw, cap, lean ? 0 : (cap < setcap ? cap : setcap) + 2, 0};   // C(0 .. ncw - 1)
   {
     constexpr int kT = CADDTREE_MAX_L * CADDTREE_MAX_K / kW;        // top-K entries per lane, at most
     float lv[kT];
@@ -722,7 +740,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   double tau = top - 3.0;
   int need = 1;                              // the tree holds at least this many nodes
   bool tight = false;                        // need is what the tree keeps before any stop test
-  if (fixed) {
+  if (lean) {                                // fixed budget, or a cost flat up to the cap
     need = cap;
     tight = true;
     tau = top - drop_fixed(need);
@@ -755,6 +773,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
     }
   }
   tau = fmin(tau, top);
+  const StopTest tst{cap, fixed, flat, c0, s.cw};
 
   int n = 0, ns = 0;
   double phi = 0.0, theta = theta0;
@@ -839,9 +858,9 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
     cc.ensure((ns < cap ? ns : cap) + 2, lane);   // C(m), C(m + 1) at every position, and C(ns + 1)
     Stop st;
     const unsigned seed = 0x9E3779B9u ^ (unsigned)b ^ ((unsigned)attempt << 16);
-    if (ns <= kW) st = stop_small(s, ns, cap, fixed, lane);
-    else if (ns <= 2 * kW) st = stop_rank<2>(s, ns, cap, fixed, lane);
-    else st = stop_hist(s, ns, cap, fixed, tau, top, lane, seed);
+    if (ns <= kW) st = stop_small(s, ns, tst, lane);
+    else if (ns <= 2 * kW) st = stop_rank<2>(s, ns, tst, lane);
+    else st = stop_hist(s, ns, tst, tau, top, lane, seed);
 
     if (!st.all) {                          // the stop (or the cap) falls inside T(tau)
       n = st.n;
@@ -860,7 +879,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       // the next pop is kept only while delta > (1 + Phi) c_{n+1} / C(n) (Lemma 1), a bound that
       // does not fall as n grows under a convex cost: aim a little below it
       double target = tau - 1.5;
-      if (!fixed) {
+      if (!lean) {
         const double c1 = s.cw[ns + 1] - s.cw[ns];
         if (c1 > 0.0) target = fmin(tau - 0.25, log((1.0 + st.phi) * c1 / s.cw[ns]) - 1.0);
       }
@@ -904,30 +923,31 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
 
 }  // namespace
 
-size_t expand_level_lds_bytes(int32_t L, int32_t K, int32_t set_cap) {
-  return level_lds_bytes((size_t)L * K, (size_t)set_cap);
+size_t expand_level_lds_bytes(int32_t L, int32_t K, int32_t set_cap, bool lean) {
+  return level_lds_bytes((size_t)L * K, (size_t)set_cap, lean);
 }
 
-int expand_level_set_cap(int32_t need) {
+int expand_level_set_cap(int32_t need, bool lean) {
+  if (lean && need > kMaxSet / 2) return kMaxLeanSet;
   int S = kSmall;
   while (S < kMaxSet && S < 2 * need) S *= 2;
   return S;
 }
 
-int expand_level_max_need() { return kMaxSet / 2; }
+int expand_level_max_need(bool lean) { return lean ? kMaxLeanSet * 4 / 5 : kMaxSet / 2; }
 
 hipError_t expand_level_prepare() {
   return hipFuncSetAttribute(reinterpret_cast<const void*>(&expand_level_kernel),
-                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                             (int)level_lds_bytes((size_t)CADDTREE_MAX_L * CADDTREE_MAX_K, kMaxSet));
+                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
 }
 
 hipError_t launch_expand_level(const ExpandArgs& a, hipStream_t stream) {
   if (a.B == 0) return hipSuccess;
+  const bool lean = a.fixed_budget || a.flat_cost;
   hipLaunchKernelGGL(expand_level_kernel, dim3((unsigned)a.B), dim3(kW),
-                     expand_level_lds_bytes(a.L, a.K, a.level_set_cap), stream, a.topk_ids, a.topk_logit, a.lse,
-                     a.L, a.K, a.cap, a.cost, a.fixed_budget ? 1 : 0, a.level_set_cap, a.token_ids, a.parent,
-                     a.depth, a.path_prob, a.n_star, a.phi, a.theta);
+                     expand_level_lds_bytes(a.L, a.K, a.level_set_cap, lean), stream, a.topk_ids, a.topk_logit,
+                     a.lse, a.L, a.K, a.cap, a.cost, a.fixed_budget ? 1 : 0, (!a.fixed_budget && a.flat_cost) ? 1 : 0,
+                     a.level_set_cap, a.token_ids, a.parent, a.depth, a.path_prob, a.n_star, a.phi, a.theta);
   return hipGetLastError();
 }
 

@@ -50,14 +50,16 @@ struct ExpandArgs {
   bool use_level;          // try the batched kernel first
   int32_t level_set_cap;   // its threshold-set capacity
   bool fixed_budget;       // no stop rule: keep the top min(cap, #nodes) nodes (DDTree)
+  bool flat_cost;          // every table holds one value: C(n) = C(0) up to the cap
 };
 size_t expand_lds_bytes(int32_t L, int32_t K, int32_t cap);
 hipError_t expand_prepare(int32_t L, int32_t K, int32_t cap);  // raises the dynamic-LDS limit once
 hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream);
 hipError_t launch_expand_level(const ExpandArgs& a, hipStream_t stream);
-size_t expand_level_lds_bytes(int32_t L, int32_t K, int32_t set_cap);
-int expand_level_set_cap(int32_t need);   // threshold-set capacity for trees of at least `need` nodes
-int expand_level_max_need();              // the largest `need` the batched kernel takes
+// (lean: fixed budgets and flat costs, which need no cost table and so hold larger sets)
+size_t expand_level_lds_bytes(int32_t L, int32_t K, int32_t set_cap, bool lean);
+int expand_level_set_cap(int32_t need, bool lean);   // threshold-set capacity for trees of at least `need` nodes
+int expand_level_max_need(bool lean);                // the largest `need` the batched kernel takes
 hipError_t expand_level_prepare();        // raises the batched kernel's dynamic-LDS limit
 
 // Stage 3: mask and position ids.

@@ -125,6 +125,7 @@ def test_expand_stage_on_oracle_inputs(name, kw):
     ("c4", dict(V=1200, B=6)),
     ("s2", dict(V=1000, B=4)),
     ("c4", dict(V=900, B=2, cost="tiny", cap=1200)),
+    ("s1", dict(V=1000, B=3)),                  # constant cost, trees of 4096 nodes
 ])
 def test_expand_paths_agree(name, kw, monkeypatch):
     """The batched expansion and the serial one give bit-identical trees."""
@@ -422,7 +423,9 @@ def test_full_c2x():
     ("c1f16", dict(V=6000, B=8)),
     ("c1f128", dict(V=6000, B=8)),              # the batched kernel's range
     ("c1f1024", dict(V=3000, B=3)),             # batched kernel, set read from LDS
-    ("c1", dict(V=2000, B=2, cap=2048, fixed=True)),   # the largest set the batched kernel holds
+    ("c1", dict(V=2000, B=2, cap=2048, fixed=True)),   # the largest set with a cost table
+    ("c1", dict(V=2000, B=2, cap=3000, fixed=True)),   # lean set (no cost table) of 5120 nodes
+    ("c1", dict(V=2000, B=2, cap=4096, fixed=True)),   # the largest budget
     ("c0", dict(fixed=True, cap=32, B=8)),      # fp32, L=4, K=4: 32 of 340 nodes
     ("c0", dict(fixed=True, L=2, K=3, cap=20, B=4, V=50)),   # 12 nodes < cap: the whole tree
 ])
