@@ -3,12 +3,14 @@
 // node i or one of its ancestors, for i, j < n_star; pos[i] = pos_offset +
 // depth[i] (the root, the bonus token, sits at pos_offset).
 //
-// Grid: (round, tile of 64 rows).  The round's parent array (indices < the
-// tile's last row) is staged in LDS; each thread produces one 32-column word of
-// one row by walking the row's ancestor chain, which is strictly decreasing in
-// the breadth-first numbering, so the walk stops as soon as it falls below the
-// word.  Packed masks store the word; dense masks expand it to 32 bytes, stored
-// as two 16-byte writes where the row allows it.
+// Grid: (round, tile of 64 rows), 256 threads.  The round's parent array
+// (indices below the tile's last row) is staged in LDS.  Two phases:
+//  1. one thread per row walks the row's ancestor chain (strictly decreasing in
+//     the breadth-first numbering) and sets each ancestor's bit in the tile's
+//     bit matrix in LDS (64 rows x up to 128 words);
+//  2. the tile is written out row by row with consecutive threads on
+//     consecutive words (packed) or 16-byte column groups (dense, each 16 bits
+//     spread to 16 bytes), so every store instruction is coalesced.
 
 #include "internal.h"
 
@@ -18,11 +20,30 @@ namespace {
 constexpr int kRows = 64;
 constexpr int kThreads = 256;
 
+// dynamic LDS: the parent array (cap int16, rounded to 16 bytes), then the tile's bit matrix
+// (kRows rows of ceil(cap / 32) words)
+__host__ __device__ inline size_t par_bytes(int cap) { return ((size_t)cap * 2 + 15) & ~(size_t)15; }
+__host__ __device__ inline size_t emit_lds_bytes(int cap) {
+  return par_bytes(cap) + (size_t)kRows * (size_t)((cap + 31) >> 5) * 4;
+}
+
+__device__ __forceinline__ int log2_pow2_at_least(int x) {   // smallest k with 2^k >= x (x >= 1)
+  int k = 0;
+  while ((1 << k) < x) ++k;
+  return k;
+}
+
+// 4 mask bits as 4 bytes of 0/1: (b * 0x00204081) & 0x01010101
+__device__ __forceinline__ uint32_t spread4(uint32_t b) { return ((b & 0xFu) * 0x00204081u) & 0x01010101u; }
+
 __global__ void __launch_bounds__(kThreads)
 emit_kernel(const int32_t* __restrict__ parent, const int32_t* __restrict__ depth,
             const int32_t* __restrict__ n_star, int cap, int pos_offset, int mask_kind,
             void* __restrict__ mask, int32_t* __restrict__ pos_ids) {
-  __shared__ int16_t par[CADDTREE_MAX_CAP];
+  extern __shared__ __align__(16) unsigned char smem[];
+  int16_t* par = reinterpret_cast<int16_t*>(smem);
+  uint32_t* tile = reinterpret_cast<uint32_t*>(smem + par_bytes(cap));   // [kRows][tw]
+  const int tw = (cap + 31) >> 5;
   const int b = blockIdx.x;
   const int n = min(max(n_star[b], 0), cap);
   const int r0 = blockIdx.y * kRows;
@@ -33,38 +54,52 @@ emit_kernel(const int32_t* __restrict__ parent, const int32_t* __restrict__ dept
   if (pos_ids)
     for (int i = r0 + (int)threadIdx.x; i < r1; i += kThreads) pos_ids[ob + i] = pos_offset + depth[ob + i];
   if (mask == nullptr || mask_kind == CADDTREE_MASK_NONE) return;
+  const int words = (n + 31) >> 5;
+  const int lw = log2_pow2_at_least(words);   // words per row, padded to a power of two
+  for (int t = threadIdx.x; t < (kRows << lw); t += kThreads) {
+    const int w = t & ((1 << lw) - 1);
+    if (w < tw) tile[(t >> lw) * tw + w] = 0u;
+  }
   __syncthreads();
 
-  const int words = (n + 31) >> 5;
-  const int items = (r1 - r0) * words;
-  for (int it = threadIdx.x; it < items; it += kThreads) {
-    const int i = r0 + it / words;
-    const int w = it - (it / words) * words;
-    const int lo = w << 5;
-    uint32_t bits = 0;
-    // the chain is strictly decreasing; a malformed parent array ends the walk
-    for (int j = i, steps = 0; j >= lo && steps <= CADDTREE_MAX_L; ++steps) {
-      if (j < lo + 32) bits |= 1u << (j - lo);
+  // 1. ancestor bits, one thread per row; the chain is strictly decreasing, and a malformed
+  //    parent array ends the walk
+  if ((int)threadIdx.x < r1 - r0) {
+    const int i = r0 + (int)threadIdx.x;
+    for (int j = i, steps = 0; j >= 0 && steps <= CADDTREE_MAX_L; ++steps) {
+      atomicOr(&tile[(i - r0) * tw + (j >> 5)], 1u << (j & 31));
       const int nj = par[j];
       if (nj >= j) break;
       j = nj;
     }
-    if (mask_kind == CADDTREE_MASK_BITS32) {
-      const int64_t stride = (cap + 31) >> 5;
-      static_cast<uint32_t*>(mask)[(ob + i) * stride + w] = bits;
-    } else {
-      uint8_t* rowp = static_cast<uint8_t*>(mask) + (ob + i) * cap;
-      const int hi = min(n, lo + 32);
-      if (hi - lo == 32 && (reinterpret_cast<uintptr_t>(rowp + lo) & 15u) == 0) {
-        // 32 bytes as two 16-byte stores; (b * 0x00204081) & 0x01010101 spreads 4 bits over 4 bytes
-        uint4 q[2];
-        uint32_t* qw = reinterpret_cast<uint32_t*>(q);
-#pragma unroll
-        for (int k = 0; k < 8; ++k) qw[k] = (((bits >> (4 * k)) & 0xFu) * 0x00204081u) & 0x01010101u;
-        reinterpret_cast<uint4*>(rowp + lo)[0] = q[0];
-        reinterpret_cast<uint4*>(rowp + lo)[1] = q[1];
+  }
+  __syncthreads();
+
+  // 2. stores
+  if (mask_kind == CADDTREE_MASK_BITS32) {
+    const int64_t stride = (cap + 31) >> 5;
+    for (int t = threadIdx.x; t < ((r1 - r0) << lw); t += kThreads) {
+      const int r = t >> lw, w = t & ((1 << lw) - 1);
+      if (w < words) static_cast<uint32_t*>(mask)[(ob + r0 + r) * stride + w] = tile[r * tw + w];
+    }
+  } else {
+    const int groups = (n + 15) >> 4;
+    const int lg = log2_pow2_at_least(groups);
+    for (int t = threadIdx.x; t < ((r1 - r0) << lg); t += kThreads) {
+      const int r = t >> lg, g = t & ((1 << lg) - 1);
+      if (g >= groups) continue;
+      const uint32_t bits = (tile[r * tw + (g >> 1)] >> ((g & 1) << 4)) & 0xFFFFu;
+      uint8_t* rowp = static_cast<uint8_t*>(mask) + (ob + r0 + r) * cap;
+      const int c0 = g << 4, c1 = min(n, c0 + 16);
+      if (c1 - c0 == 16 && (reinterpret_cast<uintptr_t>(rowp + c0) & 15u) == 0) {
+        uint4 q;
+        q.x = spread4(bits);
+        q.y = spread4(bits >> 4);
+        q.z = spread4(bits >> 8);
+        q.w = spread4(bits >> 12);
+        *reinterpret_cast<uint4*>(rowp + c0) = q;
       } else {
-        for (int j = lo; j < hi; ++j) rowp[j] = (uint8_t)((bits >> (j - lo)) & 1u);
+        for (int c = c0; c < c1; ++c) rowp[c] = (uint8_t)((bits >> (c - c0)) & 1u);
       }
     }
   }
@@ -75,7 +110,7 @@ emit_kernel(const int32_t* __restrict__ parent, const int32_t* __restrict__ dept
 hipError_t launch_emit(const EmitArgs& a, hipStream_t stream) {
   if (a.B == 0 || a.cap == 0) return hipSuccess;
   const dim3 grid((unsigned)a.B, (unsigned)((a.cap + kRows - 1) / kRows));
-  hipLaunchKernelGGL(emit_kernel, grid, dim3(kThreads), 0, stream, a.parent, a.depth, a.n_star,
+  hipLaunchKernelGGL(emit_kernel, grid, dim3(kThreads), emit_lds_bytes(a.cap), stream, a.parent, a.depth, a.n_star,
                      a.cap, a.pos_offset, (int)a.mask_kind, a.mask, a.pos_ids);
   return hipGetLastError();
 }
