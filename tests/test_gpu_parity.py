@@ -332,6 +332,17 @@ def test_full_c4():
     _full_size("c4", sorted({0, 255} | set(rng.choice(256, 6, replace=False).tolist())))
 
 
+def test_full_s2():
+    # the paper's tree sizes (n* in the hundreds, depth up to ~19): batched selection by histogram
+    rng = np.random.default_rng(5)
+    _full_size("s2", sorted({0, 255} | set(rng.choice(256, 4, replace=False).tolist())))
+
+
+def test_full_s1():
+    # a constant cost keeps every node up to the cap: 4096-node trees in the lean layout
+    _full_size("s1", [0, 131, 255])
+
+
 # ------------------------------------------------------------- context-aware cost (Sec. 4.6)
 
 def test_ctx_parity_small():
