@@ -4,13 +4,15 @@
 // depth[i] (the root, the bonus token, sits at pos_offset).
 //
 // Grid: (round, tile of 64 rows), 256 threads.  The round's parent array
-// (indices below the tile's last row) is staged in LDS.  Two phases:
+// (indices below the tile's last row) is staged in LDS with 16-byte loads.  Two
+// phases:
 //  1. one thread per row walks the row's ancestor chain (strictly decreasing in
 //     the breadth-first numbering) and sets each ancestor's bit in the tile's
 //     bit matrix in LDS (64 rows x up to 128 words);
 //  2. the tile is written out row by row with consecutive threads on
-//     consecutive words (packed) or 16-byte column groups (dense, each 16 bits
-//     spread to 16 bytes), so every store instruction is coalesced.
+//     consecutive 4-word groups (packed; single words when rows are not
+//     16-byte aligned) or 16-byte column groups (dense, each 16 bits spread to
+//     16 bytes), so every store instruction is coalesced.
 
 #include "internal.h"
 
@@ -50,21 +52,46 @@ emit_kernel(const int32_t* __restrict__ parent, const int32_t* __restrict__ dept
   if (r0 >= n) return;
   const int r1 = min(n, r0 + kRows);
   const int64_t ob = (int64_t)b * cap;
-  for (int i = threadIdx.x; i < r1; i += kThreads) par[i] = (int16_t)parent[ob + i];
+  const int nr = r1 - r0;                     // rows of this tile
+  const bool want_mask = mask != nullptr && mask_kind != CADDTREE_MASK_NONE;
+  const int32_t* pr = parent + ob;
+  const bool vec = (reinterpret_cast<uintptr_t>(pr) & 15u) == 0;
+  // 16-byte loads of whole 4-entry groups, all of a thread's groups issued at once (indices
+  // clamped, so no load waits behind a branch); the tile is cleared while they are in flight
+  static_assert(4 * 4 * kThreads >= CADDTREE_MAX_CAP, "one pass of 16-byte loads covers the largest cap");
+  const int n4 = vec ? r1 >> 2 : 0;
+  const int4* p4 = reinterpret_cast<const int4*>(pr);
+  int4 v[4];
+  if (n4 > 0) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = p4[min((int)threadIdx.x + u * kThreads, n4 - 1)];
+  }
+  if (want_mask) {                            // clear the rows in use, 16 bytes at a time
+    const int zw = nr * tw;
+    uint4* t4 = reinterpret_cast<uint4*>(tile);
+    for (int g = threadIdx.x; g < (zw >> 2); g += kThreads) t4[g] = make_uint4(0u, 0u, 0u, 0u);
+    for (int w = ((zw >> 2) << 2) + (int)threadIdx.x; w < zw; w += kThreads) tile[w] = 0u;
+  }
+  if (n4 > 0) {
+    uint2* par2 = reinterpret_cast<uint2*>(par);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int g = (int)threadIdx.x + u * kThreads;
+      if (g < n4)
+        par2[g] = make_uint2(((uint32_t)v[u].x & 0xFFFFu) | ((uint32_t)v[u].y << 16),
+                             ((uint32_t)v[u].z & 0xFFFFu) | ((uint32_t)v[u].w << 16));
+    }
+  }
+  for (int i = (n4 << 2) + (int)threadIdx.x; i < r1; i += kThreads) par[i] = (int16_t)pr[i];
   if (pos_ids)
     for (int i = r0 + (int)threadIdx.x; i < r1; i += kThreads) pos_ids[ob + i] = pos_offset + depth[ob + i];
-  if (mask == nullptr || mask_kind == CADDTREE_MASK_NONE) return;
+  if (!want_mask) return;
   const int words = (n + 31) >> 5;
-  const int lw = log2_pow2_at_least(words);   // words per row, padded to a power of two
-  for (int t = threadIdx.x; t < (kRows << lw); t += kThreads) {
-    const int w = t & ((1 << lw) - 1);
-    if (w < tw) tile[(t >> lw) * tw + w] = 0u;
-  }
   __syncthreads();
 
   // 1. ancestor bits, one thread per row; the chain is strictly decreasing, and a malformed
   //    parent array ends the walk
-  if ((int)threadIdx.x < r1 - r0) {
+  if ((int)threadIdx.x < nr) {
     const int i = r0 + (int)threadIdx.x;
     for (int j = i, steps = 0; j >= 0 && steps <= CADDTREE_MAX_L; ++steps) {
       atomicOr(&tile[(i - r0) * tw + (j >> 5)], 1u << (j & 31));
@@ -77,15 +104,38 @@ emit_kernel(const int32_t* __restrict__ parent, const int32_t* __restrict__ dept
 
   // 2. stores
   if (mask_kind == CADDTREE_MASK_BITS32) {
-    const int64_t stride = (cap + 31) >> 5;
-    for (int t = threadIdx.x; t < ((r1 - r0) << lw); t += kThreads) {
-      const int r = t >> lw, w = t & ((1 << lw) - 1);
-      if (w < words) static_cast<uint32_t*>(mask)[(ob + r0 + r) * stride + w] = tile[r * tw + w];
+    const int64_t stride = tw;
+    uint32_t* mrow = static_cast<uint32_t*>(mask) + (ob + r0) * stride;
+    if ((tw & 3) == 0 && (reinterpret_cast<uintptr_t>(mask) & 15u) == 0) {
+      // rows start on 16 bytes in LDS and in the mask: 4-word groups, one 16-byte store each
+      // (the group that holds the row's last used word stores only the used words)
+      const int gw = (words + 3) >> 2;
+      const int lg = log2_pow2_at_least(gw);   // groups per row, padded to a power of two
+      for (int t = threadIdx.x; t < (nr << lg); t += kThreads) {
+        const int r = t >> lg, g = t & ((1 << lg) - 1);
+        if (g >= gw) continue;
+        const int w = g << 2;
+        const uint4 v = *reinterpret_cast<const uint4*>(tile + r * tw + w);
+        uint32_t* dst = mrow + r * stride + w;
+        if (w + 4 <= words) {
+          *reinterpret_cast<uint4*>(dst) = v;
+        } else {
+          dst[0] = v.x;
+          if (w + 1 < words) dst[1] = v.y;
+          if (w + 2 < words) dst[2] = v.z;
+        }
+      }
+    } else {
+      const int lw = log2_pow2_at_least(words);   // words per row, padded to a power of two
+      for (int t = threadIdx.x; t < (nr << lw); t += kThreads) {
+        const int r = t >> lw, w = t & ((1 << lw) - 1);
+        if (w < words) mrow[r * stride + w] = tile[r * tw + w];
+      }
     }
   } else {
     const int groups = (n + 15) >> 4;
     const int lg = log2_pow2_at_least(groups);
-    for (int t = threadIdx.x; t < ((r1 - r0) << lg); t += kThreads) {
+    for (int t = threadIdx.x; t < (nr << lg); t += kThreads) {
       const int r = t >> lg, g = t & ((1 << lg) - 1);
       if (g >= groups) continue;
       const uint32_t bits = (tile[r * tw + (g >> 1)] >> ((g & 1) << 4)) & 0xFFFFu;
