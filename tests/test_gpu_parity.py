@@ -292,6 +292,29 @@ def test_determinism():
             assert np.array_equal(a[k], b[k]), k
 
 
+# ------------------------------------------------------------- seeded random shapes
+
+def random_case(i):
+    """A seeded random small workload: any L, K, V, cap, dtype, mask and cost family the plan accepts,
+    a fixed budget now and then, padded rows and a position offset."""
+    rng = np.random.default_rng(7000 + i)
+    base = synth.get_config(("c0", "c1", "c3", "s2")[i % 4])
+    K = int(rng.integers(1, 17))
+    cfg = base.replace(
+        name=f"rand{i}", B=int(rng.integers(1, 7)), L=int(rng.integers(1, 33)), K=K,
+        V=int(rng.integers(max(K, 2), 6001)), cap=int(rng.integers(0, 701)),
+        dtype=("f32", "bf16")[int(rng.integers(0, 2))], mask=("u8", "bits")[int(rng.integers(0, 2))],
+        cost=str(rng.choice(["c0", "c1", "c3", "c4", "const", "tiny"])), fixed=bool(rng.random() < 0.2),
+        seed=synth.configs.SEED_BASE + 7000 + i)
+    return cfg, int(rng.integers(0, 100)), int(rng.choice([0, 0, 1, 3, 8]))
+
+
+@pytest.mark.parametrize("i", range(48))
+def test_random_shapes(i):
+    cfg, pos_offset, pad = random_case(i)
+    _parity_batch(cfg, list(range(cfg.B)), pos_offset=pos_offset, pad=pad)
+
+
 # ------------------------------------------------------------- full-size workloads
 
 def _full_size(name, sample, workers=16):
