@@ -62,6 +62,7 @@
 #include <cmath>
 
 #include "expand_common.h"
+#include "expand_serial.h"
 #include "internal.h"
 
 namespace caddtree {
@@ -684,13 +685,18 @@ __device__ double raise_tau(const Lds& s, int& la, int& lb, int K, double Ad, do
   return t2;
 }
 
+// A round the batched form cannot settle, run by the serial form in the same workgroup (the
+// launch reserved LDS for the serial layout).  Out of line: it is rare, and inlined it would
+// crowd the batched kernel's registers.
+__device__ __attribute__((noinline)) void serial_in_place(serial::Args a, int b) { serial::expand_round(a, b); }
+
 __global__ void __launch_bounds__(kW)
 expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict__ topk_logit,
                     const double* __restrict__ lse, int L, int K, int cap, CostTables ct, int fixed,
                     int flat, int setcap, int32_t* __restrict__ token_ids,
                     int32_t* __restrict__ parent_out, int32_t* __restrict__ depth_out,
                     float* __restrict__ path_prob, int32_t* __restrict__ n_star_out,
-                    float* __restrict__ phi_out, float* __restrict__ theta_out) {
+                    float* __restrict__ phi_out, float* __restrict__ theta_out, int in_place) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int b = blockIdx.x;
   const int lane = threadIdx.x;
@@ -759,7 +765,12 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       tight = true;
       tau = top - drop_fixed(need);
     } else if (m0 < 0 || m0 >= setcap / 2) {
-      if (lane == 0) n_star_out[b] = -1;    // flat for longer than the set holds: the serial kernel's case
+      // flat for longer than the set holds: the serial form's case
+      if (in_place)
+        serial_in_place(serial::Args{topk_ids, topk_logit, lse, L, K, cap, ct, fixed, token_ids, parent_out,
+                                     depth_out, path_prob, n_star_out, phi_out, theta_out}, b);
+      else if (lane == 0)
+        n_star_out[b] = -1;
       return;
     } else {
       need = m0 + 1;
@@ -887,8 +898,12 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
     }
     if (done) theta = n == 0 ? theta0 : (1.0 + phi) / rc(n);
   }
-  if (!done) {
-    if (lane == 0) n_star_out[b] = -1;      // left to the serial kernel
+  if (!done) {                              // left to the serial form
+    if (in_place)
+      serial_in_place(serial::Args{topk_ids, topk_logit, lse, L, K, cap, ct, fixed, token_ids, parent_out,
+                                   depth_out, path_prob, n_star_out, phi_out, theta_out}, b);
+    else if (lane == 0)
+      n_star_out[b] = -1;
     return;
   }
   if (lane == 0) {
@@ -941,13 +956,15 @@ hipError_t expand_level_prepare() {
                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
 }
 
-hipError_t launch_expand_level(const ExpandArgs& a, hipStream_t stream) {
+hipError_t launch_expand_level(const ExpandArgs& a, size_t in_place_lds, hipStream_t stream) {
   if (a.B == 0) return hipSuccess;
   const bool lean = a.fixed_budget || a.flat_cost;
-  hipLaunchKernelGGL(expand_level_kernel, dim3((unsigned)a.B), dim3(kW),
-                     expand_level_lds_bytes(a.L, a.K, a.level_set_cap, lean), stream, a.topk_ids, a.topk_logit,
+  size_t lds = expand_level_lds_bytes(a.L, a.K, a.level_set_cap, lean);
+  if (in_place_lds > lds) lds = in_place_lds;
+  hipLaunchKernelGGL(expand_level_kernel, dim3((unsigned)a.B), dim3(kW), lds, stream, a.topk_ids, a.topk_logit,
                      a.lse, a.L, a.K, a.cap, a.cost, a.fixed_budget ? 1 : 0, (!a.fixed_budget && a.flat_cost) ? 1 : 0,
-                     a.level_set_cap, a.token_ids, a.parent, a.depth, a.path_prob, a.n_star, a.phi, a.theta);
+                     a.level_set_cap, a.token_ids, a.parent, a.depth, a.path_prob, a.n_star, a.phi, a.theta,
+                     in_place_lds > 0 ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -55,7 +55,12 @@ struct ExpandArgs {
 size_t expand_lds_bytes(int32_t L, int32_t K, int32_t cap);
 hipError_t expand_prepare(int32_t L, int32_t K, int32_t cap);  // raises the dynamic-LDS limit once
 hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream);
-hipError_t launch_expand_level(const ExpandArgs& a, hipStream_t stream);
+// in_place_lds > 0: a round the batched kernel cannot settle is run by the serial form in the
+// same workgroup, in that many bytes of LDS (the launch reserves the larger of the two layouts);
+// 0: such a round is flagged (n_star = -1) for the serial kernel
+hipError_t launch_expand_level(const ExpandArgs& a, size_t in_place_lds, hipStream_t stream);
+// the largest serial layout that the batched kernel reserves LDS for
+constexpr size_t kInPlaceLds = 64 * 1024;
 // (lean: fixed budgets and flat costs, which need no cost table and so hold larger sets)
 size_t expand_level_lds_bytes(int32_t L, int32_t K, int32_t set_cap, bool lean);
 int expand_level_set_cap(int32_t need, bool lean);   // threshold-set capacity for trees of at least `need` nodes

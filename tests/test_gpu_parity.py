@@ -99,7 +99,9 @@ def _oracle_tables(cfg, rs):
     ("s1", dict(V=1500, B=2)),                         # constant cost: grows to the 4096 cap
     ("s2", dict(V=1500, B=3)),                         # cold marginals: deep trees
     ("c4", dict(V=800, B=4, cost="const", cap=700)),   # heap sizes far past the LDS fast cases
-    ("c4", dict(V=900, B=3, cost="tiny", cap=1500)),   # rising cost, trees too large for the batched kernel
+    ("c4", dict(V=900, B=3, cost="tiny", cap=1500)),   # rising cost, trees too large for the batched kernel:
+                                                       # the serial form runs in place (its LDS fits)
+    ("c4", dict(V=900, B=2, cost="tiny", cap=4096)),   # the same with a 4096 cap: flagged for the serial kernel
 ])
 def test_expand_stage_on_oracle_inputs(name, kw):
     """Algorithm 1 alone, fed the oracle's own top-K table and fp64 normalisers: no guard needed."""
