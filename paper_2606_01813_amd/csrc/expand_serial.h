@@ -41,8 +41,6 @@
 // children of a kept node are ranks 0 .. c-1, since a kept node's
 // predecessors are kept).
 
-#include <cmath>
-#include <type_traits>
 #pragma once
 
 #include <cmath>
@@ -52,7 +50,6 @@
 
 namespace caddtree {
 namespace serial {
-
 
 constexpr int kThreads = 64;
 constexpr int kSlots = 4;                  // register frontier capacity = 256 entries
