@@ -46,9 +46,10 @@
 // nodes, start well below and let the in-place raise bring the set to size.
 // A round that does not settle within kMaxAttempts (or kMaxRaises raises in
 // one attempt), or whose tree needs more nodes than the set holds (512, or up
-// to 4096 for fixed budgets and long flat cost starts, sized by the host), is
-// flagged (n_star = -1) and left to the serial kernel, which gives the same
-// tree.
+// to 4096 for fixed budgets and long flat cost starts, sized by the host), goes
+// to the serial form (expand_serial.h), which gives the same tree: run in place
+// by the same workgroup when the launch reserved LDS for the serial layout,
+// else flagged (n_star = -1) for the serial kernel.
 //
 // The kept nodes are a prefix of the pop order and a prefix-closed set, so
 // their breadth-first positions are a running count over generation order.
