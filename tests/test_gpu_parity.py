@@ -294,6 +294,46 @@ def test_determinism():
             assert np.array_equal(a[k], b[k]), k
 
 
+# ------------------------------------------------------------- HIP graph capture
+
+def test_build_under_graph_capture():
+    """caddtree_build enqueues kernels only (no allocation, memset or synchronisation), so a caller
+    can capture it in a HIP graph; every replay must equal the eager build, with eager work and
+    synchronisations between the replays."""
+    import torch
+    cfg = synth.get_config("c1").replace(V=5000, B=8, mask="bits")
+    xs = synth.draw_batch(cfg)
+    plan = make_plan(cfg)
+    lg = torch_logits(cfg, xs)
+    ref = host(run_build(plan, lg))
+    out = plan.new_outputs(cfg.B)
+    ws = plan.new_workspace(cfg.B)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):                # warm-up outside the capture
+        plan.build(lg, out, workspace=ws, stream=torch.cuda.current_stream())
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        plan.build(lg, out, workspace=ws, stream=torch.cuda.current_stream())
+    for rep in range(3):
+        for t in (out.n_star, out.token_ids, out.parent, out.depth, out.mask):
+            t.fill_(-9)
+        run_build(plan, lg)                      # eager work between the replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        h = host(out)
+        assert np.array_equal(h["n_star"], ref["n_star"]), f"replay {rep}: n_star"
+        for i, n in enumerate(ref["n_star"]):
+            for k in ("token_ids", "parent", "depth", "pos_ids", "path_prob"):
+                assert np.array_equal(h[k][i, :n], ref[k][i, :n]), f"replay {rep}: round {i} {k}"
+            w = (n + 31) // 32
+            assert np.array_equal(h["mask"][i, :n, :w], ref["mask"][i, :n, :w]), f"replay {rep}: round {i} mask"
+        say(f"[graph] replay {rep}: equal to the eager build; n* = {h['n_star'].tolist()}")
+
+
 # ------------------------------------------------------------- seeded random shapes
 
 def random_case(i):
