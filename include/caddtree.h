@@ -159,7 +159,10 @@ typedef struct {
 /* The whole hot path for B rounds: reduce + top-K, expansion, emission.
  * logits: DEVICE [B, L, row_stride] of the plan's dtype; B >= 0 (0 is a no-op).
  * workspace: DEVICE, >= caddtree_workspace_bytes(plan, B) bytes, 256-byte aligned
- * (may be NULL when every top-K output pointer is given). */
+ * (may be NULL when every top-K output pointer is given).
+ * The call only enqueues kernels on `stream` (no allocation, memset or
+ * synchronisation), so it may be captured in a HIP graph; a replay reads and
+ * writes the buffers given at capture. */
 caddtree_status_t caddtree_build(caddtree_plan_t plan, const void* logits, int64_t B, int64_t row_stride,
                                  int32_t pos_offset, const int64_t* ctx_len, const caddtree_outputs_t* out,
                                  void* workspace, size_t workspace_bytes, hipStream_t stream);
