@@ -54,6 +54,13 @@ EXPORTS = [
 def load(path: str = LIB_PATH) -> ctypes.CDLL:
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build the HIP library first (__graft_entry__.build())")
+    # PyTorch-ROCm ships its own HIP runtime under the same soname (libamdhip64.so.7).  Importing
+    # torch first makes this library bind to that runtime, so the tensors' memory and streams and
+    # the kernels share one runtime; in the other order torch would later find no GPU.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     lib.caddtree_plan_create.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(vp)]

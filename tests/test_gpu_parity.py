@@ -294,6 +294,36 @@ def test_determinism():
             assert np.array_equal(a[k], b[k]), k
 
 
+# ------------------------------------------------------------- process set-up
+
+def test_plan_before_torch_in_a_fresh_process():
+    """PyTorch-ROCm bundles its own HIP runtime under the soname the library links; the binding
+    imports torch before loading the library so that both use that one runtime.  A fresh process
+    that creates a plan first and touches torch afterwards must still see the GPU and build."""
+    import os
+    import subprocess
+    import sys
+    import textwrap
+    code = textwrap.dedent('''
+        import numpy as np
+        from paper_2606_01813_amd import Plan
+        plan = Plan(L=4, V=1024, K=4, cap=32, t_draft=1.0, t_verify=1.0 + 0.01 * np.arange(33), dtype="f32")
+        import torch
+        assert torch.cuda.is_available(), "torch lost the GPU"
+        x = torch.randn(2, 4, 1024, device="cuda")
+        out = plan.new_outputs(2)
+        plan.build(x, out, workspace=plan.new_workspace(2))
+        torch.cuda.synchronize()
+        n = out.n_star.tolist()
+        assert all(1 <= v <= 32 for v in n), n
+        print("n_star", n)
+    ''')
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=300)
+    say(f"[process] {r.stdout.strip()}")
+    assert r.returncode == 0, r.stderr[-3000:]
+
+
 # ------------------------------------------------------------- HIP graph capture
 
 def test_build_under_graph_capture():
