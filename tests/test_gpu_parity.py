@@ -390,7 +390,8 @@ def test_random_shapes(i):
 # ------------------------------------------------------------- full-size workloads
 
 def _full_size(name, sample, workers=16):
-    cfg = synth.get_config(name)
+    cfg = synth.get_config(name) if isinstance(name, str) else name
+    name = cfg.name
     attempts, _, rs = _guard.guarded_batch(cfg, sample)
     say(f"[full] {name}: B={cfg.B} L={cfg.L} V={cfg.V} {cfg.dtype}; guarded sample {sample} "
         f"redraws={sum(attempts.values())}")
@@ -425,6 +426,14 @@ def test_full_c3():
 def test_full_c4():
     rng = np.random.default_rng(4)
     _full_size("c4", sorted({0, 255} | set(rng.choice(256, 6, replace=False).tolist())))
+
+
+def test_many_rounds():
+    # more rounds than a grid dimension of 65535 blocks: the expansion and emission grids run
+    # one block per round along x
+    cfg = synth.get_config("c0").replace(name="many", B=70000, L=2, V=40, K=2, cap=6)
+    rng = np.random.default_rng(6)
+    _full_size(cfg, sorted({0, 65535, 65536, 69999} | set(rng.choice(70000, 12, replace=False).tolist())))
 
 
 def test_full_s2():
