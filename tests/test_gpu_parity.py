@@ -54,6 +54,8 @@ SMALL = [
     ("c3", dict(V=30011, B=6)),                                         # temperature mix, packed mask
     ("c4", dict(V=3000, B=4)),                                          # L=32, K=16, cap 4096, fp32
     ("c4", dict(V=64, B=4, K=16, L=32)),                                # V = one fp32 chunk
+    ("c0", dict(V=5, K=5, L=3, cap=200, B=6)),                          # every token in the top-K
+    ("c1", dict(V=16, K=16, L=4, cap=600, B=4, cost="tiny")),           # the same in bf16, trees past 512
 ]
 
 
