@@ -326,6 +326,50 @@ def test_plan_before_torch_in_a_fresh_process():
     assert r.returncode == 0, r.stderr[-3000:]
 
 
+# ------------------------------------------------------------- concurrency
+
+def test_concurrent_builds_on_two_streams():
+    """One plan, two host threads, each building on its own stream into its own outputs and
+    workspace, with no synchronisation between them: every result equals the build done alone
+    (a plan is immutable; the last-error string is per thread)."""
+    import threading
+    import torch
+    cfg = synth.get_config("c1").replace(V=6000, B=6)
+    plan = make_plan(cfg)
+    inputs = [torch_logits(cfg, synth.draw_batch(cfg.replace(seed=cfg.seed + k))) for k in range(2)]
+    refs = [host(run_build(plan, lg)) for lg in inputs]
+    outs = [plan.new_outputs(cfg.B) for _ in range(2)]
+    wss = [plan.new_workspace(cfg.B) for _ in range(2)]
+    streams = [torch.cuda.Stream() for _ in range(2)]
+    torch.cuda.synchronize()
+    errors = []
+
+    def worker(k):
+        try:
+            with torch.cuda.stream(streams[k]):
+                for _ in range(20):
+                    plan.build(inputs[k], outs[k], workspace=wss[k], stream=streams[k])
+        except Exception as e:   # noqa: BLE001 (reported below)
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=worker, args=(k,)) for k in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for k in range(2):
+        h = host(outs[k])
+        assert np.array_equal(h["n_star"], refs[k]["n_star"]), f"stream {k}: n_star"
+        for i, n in enumerate(refs[k]["n_star"]):
+            for key in ("token_ids", "parent", "depth", "pos_ids"):
+                assert np.array_equal(h[key][i, :n], refs[k][key][i, :n]), f"stream {k}: round {i} {key}"
+            assert np.array_equal(h["mask"][i, :n, :n], refs[k]["mask"][i, :n, :n]), f"stream {k}: round {i} mask"
+    say(f"[streams] two threads x 20 builds: equal to the single builds; n* {refs[0]['n_star'].tolist()} "
+        f"{refs[1]['n_star'].tolist()}")
+
+
 # ------------------------------------------------------------- HIP graph capture
 
 def test_build_under_graph_capture():
