@@ -326,6 +326,23 @@ def test_plan_before_torch_in_a_fresh_process():
     assert r.returncode == 0, r.stderr[-3000:]
 
 
+# ------------------------------------------------------------- optional outputs
+
+def test_workspace_topk_and_no_mask():
+    """Without top-K outputs the table lives in the workspace, and a plan may emit no mask: the
+    tree is the same as with every output requested."""
+    cfg = synth.get_config("c3").replace(V=7000, B=6)
+    lg = torch_logits(cfg, synth.draw_batch(cfg))
+    full = host(run_build(make_plan(cfg), lg, topk=True))
+    bare = host(run_build(make_plan(cfg, mask="none"), lg, topk=False))
+    assert bare["mask"] is None and bare["topk_ids"] is None
+    assert np.array_equal(bare["n_star"], full["n_star"])
+    for i, n in enumerate(full["n_star"]):
+        for k in ("token_ids", "parent", "depth", "pos_ids", "path_prob"):
+            assert np.array_equal(bare[k][i, :n], full[k][i, :n]), f"round {i} {k}"
+    assert np.array_equal(bare["phi"], full["phi"]) and np.array_equal(bare["theta"], full["theta"])
+
+
 # ------------------------------------------------------------- concurrency
 
 def test_concurrent_builds_on_two_streams():
