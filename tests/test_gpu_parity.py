@@ -326,6 +326,30 @@ def test_plan_before_torch_in_a_fresh_process():
     assert r.returncode == 0, r.stderr[-3000:]
 
 
+# ------------------------------------------------------------- degenerate logits
+
+@pytest.mark.parametrize("kw", [
+    dict(cost="const", cap=100, fixed=False),   # grows to the cap through a tie group of 256
+    dict(cost="c4", cap=100, fixed=True),       # fixed budget through the same ties
+    dict(cost="const", cap=340, fixed=False),   # the whole tree (4 + 16 + 64 + 256 nodes)
+])
+def test_constant_logits(kw):
+    """Every logit equal: all nodes of a depth tie on sigma and Lambda, so the pop order inside a
+    depth is the rank tuple alone, and the cap cuts a group of equal nodes.  No decision depends on
+    the normaliser's rounding (depths differ by ln V in sigma; a flat cost or a fixed budget never
+    stops before the cap), so the oracle's tree is compared without the input guard."""
+    cfg = synth.get_config("c0").replace(B=3, L=4, V=1000, K=4, dtype="f32", mask="bits", **kw)
+    x = np.zeros((cfg.B, cfg.L, cfg.V), dtype=np.float32)
+    x[1] += 2.5                                   # a constant shift changes nothing
+    x[2] -= 7.0
+    rs = [_guard.oracle_round(cfg, x[b], b=b) for b in range(cfg.B)]
+    plan = make_plan(cfg)
+    h = host(run_build(plan, torch_logits(cfg, x)))
+    compare_topk(h, rs)
+    compare_tree(h, rs, cfg.mask, cfg.cap)
+    say(f"[constant] {kw}: n* {[r.n_star for r in rs]}")
+
+
 # ------------------------------------------------------------- optional outputs
 
 def test_workspace_topk_and_no_mask():
