@@ -350,6 +350,32 @@ def test_constant_logits(kw):
     say(f"[constant] {kw}: n* {[r.n_star for r in rs]}")
 
 
+def test_certain_tokens():
+    """One token per position 100 nats above the rest: its log q rounds to 0, so the chain of those
+    tokens has sigma = 0 at every depth (the clamp of the prefix probability) and the chain pops in
+    depth order.  The stage gets the oracle's own tables (exact); the whole path, whose normaliser
+    may differ from the oracle's by a few ulps, must give the same tree."""
+    import torch
+    cfg = synth.get_config("c1").replace(B=4, V=3000, dtype="f32", mask="u8")
+    rng = np.random.default_rng(9)
+    x = (rng.standard_normal((cfg.B, cfg.L, cfg.V)) * 0.5).astype(np.float32)
+    peak = rng.integers(0, cfg.V, size=(cfg.B, cfg.L))
+    x[np.arange(cfg.B)[:, None], np.arange(cfg.L)[None, :], peak] = 100.0
+    rs = [_guard.oracle_round(cfg, x[b], b=b) for b in range(cfg.B)]
+    for r in rs:
+        assert r.n_star >= cfg.L and np.all(r.tree.depth[:cfg.L] == np.arange(1, cfg.L + 1))
+    plan = make_plan(cfg)
+    out = plan.new_outputs(cfg.B)
+    ids, logit, lse = _oracle_tables(cfg, rs)
+    plan.expand(ids, logit, lse, out)
+    plan.emit(out, pos_offset=0)
+    torch.cuda.synchronize()
+    compare_tree(host(out), rs, cfg.mask, cfg.cap, prob_rtol=1e-6)
+    h = host(run_build(plan, torch_logits(cfg, x)))
+    compare_tree(h, rs, cfg.mask, cfg.cap)
+    say(f"[certain] n* {[r.n_star for r in rs]}")
+
+
 # ------------------------------------------------------------- optional outputs
 
 def test_workspace_topk_and_no_mask():
