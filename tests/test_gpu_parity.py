@@ -56,6 +56,8 @@ SMALL = [
     ("c4", dict(V=64, B=4, K=16, L=32)),                                # V = one fp32 chunk
     ("c0", dict(V=5, K=5, L=3, cap=200, B=6)),                          # every token in the top-K
     ("c1", dict(V=16, K=16, L=4, cap=600, B=4, cost="tiny")),           # the same in bf16, trees past 512
+    ("c1", dict(V=262144, L=4, B=2)),                                   # a larger vocabulary, whole chunks only
+    ("c4", dict(V=131072, L=3, B=2)),                                   # the same in fp32
 ]
 
 
