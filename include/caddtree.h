@@ -61,7 +61,7 @@ extern "C" {
 typedef enum {
   CADDTREE_OK = 0,
   CADDTREE_E_INVALID = 1,      /* bad argument: NULL where required, negative or inconsistent size */
-  CADDTREE_E_UNSUPPORTED = 2,  /* valid request beyond this build's limits (L, K, cap, V) */
+  CADDTREE_E_UNSUPPORTED = 2,  /* valid request beyond the library's limits (L, K, cap, V) */
   CADDTREE_E_COST = 3,         /* cost model rejected: C_d <= 0, non-finite, C_v decreasing or not convex */
   CADDTREE_E_WORKSPACE = 4,    /* workspace NULL, misaligned or smaller than caddtree_workspace_bytes() */
   CADDTREE_E_HIP = 5           /* a HIP runtime call or kernel launch failed */

@@ -53,7 +53,7 @@ EXPORTS = [
 
 def load(path: str = LIB_PATH) -> ctypes.CDLL:
     if not os.path.exists(path):
-        raise ImportError(f"{path} is missing: build the HIP library first (__graft_entry__.build())")
+        raise ImportError(f"{path} is missing: build the HIP library first (python -m paper_2606_01813_amd._build)")
     # PyTorch-ROCm ships its own HIP runtime under the same soname (libamdhip64.so.7).  Importing
     # torch first makes this library bind to that runtime, so the tensors' memory and streams and
     # the kernels share one runtime; in the other order torch would later find no GPU.
