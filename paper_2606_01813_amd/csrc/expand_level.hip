@@ -893,7 +893,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       double target = tau - 1.5;
       if (!lean) {
         const double c1 = s.cw[ns + 1] - s.cw[ns];
-        if (c1 > 0.0) target = fmin(tau - 0.25, log((1.0 + st.phi) * c1 / s.cw[ns]) - 1.0);
+        if (c1 > 0.0) target = fmin(tau - 0.25, log((1.0 + st.phi) * c1 / s.cw[ns]) - 1.5);
       }
       tau = target;
     }
