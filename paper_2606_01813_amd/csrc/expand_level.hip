@@ -79,7 +79,7 @@ constexpr int kMaxAttempts = 12;
 constexpr int kBins = kW;             // histogram bins of the in-place raise (one per lane)
 constexpr int kRefine = 4;            // histogram passes per raise
 constexpr int kMaxRaises = 32;        // raises per attempt
-constexpr double kDropFlat = 3.0;     // a flat start begins this far (nats) below the cost-model threshold
+constexpr double kDropFlat = 2.0;     // a flat start begins this far (nats) below the cost-model threshold
 
 // Fixed budgets and costs flat up to the cap keep `need` nodes: the first threshold lies this far
 // (nats) below the top node, further for larger trees.
