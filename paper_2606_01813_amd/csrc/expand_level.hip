@@ -797,7 +797,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
     // before any stop test, else room for a stop past need
     int keep_hi;
     if (tight) {
-      keep_hi = need + need / 4 + 32;
+      keep_hi = need + need / 8 + 16;
     } else {
       const int half = setcap / 2, mid = (need + setcap) / 2;
       keep_hi = need <= 1 || half > mid ? half : mid;
