@@ -34,7 +34,7 @@ Precision: fp64 throughout (bf16 and fp32 logits are widened exactly).
 from .vocab import widen, log_normalizer, top_k, marginals
 from .alg1 import expand, Expansion
 from .layout import canonical_order, emit_mask, TreeOut
-from .pipeline import build_round, RoundResult, decision_margins
+from .pipeline import build_round, RoundResult, Margins, decision_margins
 from .cost import context_cost
 from . import accept, costfit
 
@@ -42,6 +42,6 @@ __all__ = [
     "widen", "log_normalizer", "top_k", "marginals",
     "expand", "Expansion",
     "canonical_order", "emit_mask", "TreeOut",
-    "build_round", "RoundResult", "decision_margins",
+    "build_round", "RoundResult", "Margins", "decision_margins",
     "context_cost", "accept", "costfit",
 ]

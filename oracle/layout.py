@@ -79,9 +79,7 @@ def emit_mask(parent: np.ndarray, kind: str = "u8", cap: int | None = None) -> n
         cap = n if cap is None else cap
         words = (cap + 31) // 32
         out = np.zeros((n, words), dtype=np.uint32)
-        for i in range(n):
-            for j in range(n):
-                if dense[i, j]:
-                    out[i, j // 32] |= np.uint32(1) << np.uint32(j % 32)
+        for j in range(n):          # column j sets bit j % 32 of word j // 32 in every row
+            out[:, j // 32] |= dense[:, j].astype(np.uint32) << np.uint32(j % 32)
         return out
     raise ValueError(kind)

@@ -4,25 +4,31 @@
 per-position marginals and top-K (Sec. 3.2), Algorithm 1 (Sec. 4.5), and the
 tree layout with its attention mask and position ids (Sec. 3.3).
 
-``decision_margins`` measures how close a round sits to a decision boundary,
-for the input guard that keeps floating-point decisions unambiguous:
+``decision_margins`` lists every floating-point decision of a round with its
+distance from a tie, for the input guard that keeps such decisions unambiguous.
+A GPU log-normaliser LSE_i may differ from the oracle's by a tiny error e_i;
+that shifts sigma at depth d by -(e_1 + .. + e_d).  So each margin comes with
+its depth span, the number of normalisers whose error it can carry:
 
-* stop margins: at every tested pop, Lemma 1 (eq. stopping) says the node is
-  kept iff delta * C(n) > (1 + Phi) * c_{n+1}, where c_{n+1} = C(n+1) - C(n);
-  the margin is |delta C(n) - (1 + Phi) c_{n+1}| / (delta C(n) + (1 + Phi)
-  c_{n+1}), and 1 when c_{n+1} = 0 (the node is always kept then);
-* cross-depth gap: a perturbation of the log-normalisers shifts every sigma at
-  depth d by the same amount, so the kept set can only change through a
-  comparison between a kept node and a frontier node at a different depth;
-  the gap is min over depths d != d' of (min sigma of kept nodes at d) - (max
-  sigma of frontier nodes at d').
+* stop margins: at every stop test, Lemma 1 (eq. stopping) keeps the node iff
+  delta * C(n) > (1 + Phi) * c_{n+1}, where c_{n+1} = C(n+1) - C(n); the
+  margin is |delta C(n) - (1 + Phi) c_{n+1}| / (delta C(n) + (1 + Phi)
+  c_{n+1}) (no margin when c_{n+1} = 0: the node is always kept then).  delta
+  carries the error of the tested node's depth and Phi that of the deepest
+  node kept so far; the span is the larger of the two depths;
+* cross-depth gaps: the selected set can change only through a comparison
+  between a selected node and a frontier node (an unselected node that would
+  come next along its branch) at a different depth, since same-depth
+  comparisons reduce to the raw-logit sums Lambda, which carry no normaliser.
+  For depths d != d' the gap is (min sigma of selected nodes at d) - (max sigma
+  of frontier nodes at d'), with span |d - d'|.
 """
 
 from __future__ import annotations
 
 import dataclasses
 import math
-from typing import Optional
+from typing import List, Optional, Tuple
 
 import numpy as np
 
@@ -53,25 +59,40 @@ def build_round(logits: np.ndarray, dtype: str, K: int, t_draft: float, t_verify
     return RoundResult(marg, ex, tree, m)
 
 
-def decision_margins(ex: Expansion):
-    """Returns (min stop margin over tested pops, min cross-depth gap); inf if none apply."""
-    stop = math.inf
+@dataclasses.dataclass
+class Margins:
+    stop: List[Tuple[float, int]]     # (relative stop margin, depth span), one per stop test
+    cross: List[Tuple[float, int]]    # (sigma gap, depth span), one per pair of depths
+
+    @property
+    def min_stop(self) -> float:
+        return min((m for m, _ in self.stop), default=math.inf)
+
+    @property
+    def min_gap(self) -> float:
+        return min((g for g, _ in self.cross), default=math.inf)
+
+
+def decision_margins(ex: Expansion) -> Margins:
+    stop = []
+    deepest = 0
     for s in ex.steps:
         c = s.c_next - s.c_n
-        if c == 0.0:
-            continue
-        a = s.delta * s.c_n
-        b = (1.0 + s.phi) * c
-        stop = min(stop, abs(a - b) / (abs(a) + abs(b)))
+        if c != 0.0:
+            a = s.delta * s.c_n
+            b = (1.0 + s.phi) * c
+            stop.append((abs(a - b) / (abs(a) + abs(b)), max(s.depth, deepest)))
+        if s.kept:
+            deepest = max(deepest, s.depth)
     kept_min = {}
     for nd in ex.selected:
         kept_min[nd.depth] = min(kept_min.get(nd.depth, math.inf), nd.sigma)
     front_max = {}
     for nd in ex.frontier:
         front_max[nd.depth] = max(front_max.get(nd.depth, -math.inf), nd.sigma)
-    gap = math.inf
+    cross = []
     for d, lo in kept_min.items():
         for d2, hi in front_max.items():
             if d2 != d:
-                gap = min(gap, lo - hi)
-    return stop, gap
+                cross.append((lo - hi, abs(d - d2)))
+    return Margins(stop, cross)

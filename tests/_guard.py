@@ -1,13 +1,16 @@
 """Input guard: redraw rounds whose tree decisions sit within a hair of a tie.
 
-A GPU log-normaliser differs from the oracle's fp64 value by rounding, which
-shifts every log prefix probability at depth d by the same tiny amount.  Such a
-shift can only change the output through a stop decision or a kept-versus-
-frontier comparison across depths whose margin is below it.  The guard keeps
-every such margin of a round at or above ``TAU`` (relative; 1e-6 is the gap the
-workloads require), redrawing the round with the next attempt of its seed
-until it passes.  Same-depth comparisons are exact on both sides and need no
-guard.
+A GPU log-normaliser LSE_i differs from the oracle's fp64 value by at most
+``LSE_ATOL`` (the parity tests check it), and the log prefix probability of a
+depth-d node carries the sum of d such errors.  So a stop decision or a
+selected-versus-frontier comparison between depths d and d' can flip only if
+its margin is below span * LSE_ATOL, with span the depth (stop) or |d - d'|
+(comparison) that ``oracle.decision_margins`` reports.  The guard keeps every
+margin of a round at or above max(TAU, 2 * span * LSE_ATOL): TAU = 1e-6 is
+the gap the workloads require, and the factor 2 leaves headroom for the
+relative form of the stop margin.  A round that fails is redrawn with the next
+attempt of its seed.  Same-depth comparisons are exact on both sides and need
+no guard.
 """
 
 from __future__ import annotations
@@ -18,9 +21,19 @@ import numpy as np
 
 import oracle
 import synth
+from tests._parity import LSE_ATOL
 
 TAU = 1e-6
 MAX_ATTEMPTS = 20
+
+
+def required(span: int, tau: float = TAU) -> float:
+    """The margin a decision whose error can reach span normalisers must keep."""
+    return max(tau, 2.0 * span * LSE_ATOL)
+
+
+def clears(m: "oracle.Margins", tau: float = TAU) -> bool:
+    return all(v >= required(span, tau) for v, span in m.stop + m.cross)
 
 
 _CTX_CACHE: Dict[Tuple[str, int], Tuple[np.ndarray, np.ndarray, np.ndarray]] = {}
@@ -54,8 +67,7 @@ def guarded_round(cfg: synth.Config, b: int, tau: float = TAU, pos_offset: int =
     for a in range(MAX_ATTEMPTS):
         x = synth.draw_round(cfg, b, a)
         r = oracle_round(cfg, x, pos_offset, b=b)
-        stop, gap = oracle.decision_margins(r.exp)
-        if stop >= tau and gap >= tau:
+        if clears(oracle.decision_margins(r.exp), tau):
             return a, x, r
     raise RuntimeError(f"round {b} of {cfg.name} failed the guard {MAX_ATTEMPTS} times")
 

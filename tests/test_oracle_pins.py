@@ -11,6 +11,8 @@
 * Monte-Carlo: Phi(T) is the expected accepted length under the drafter's
   factorised joint (eq. surrogate);
 * mask invariants;
+* the decision margins of the hand-worked round (tests/golden/hand_example_margins.json),
+  which the input guard uses to pick the rounds the parity tests compare;
 * planted mistakes: each mutation of the oracle below fails one of the pins.
 """
 
@@ -137,6 +139,24 @@ def check_topk_ties():
     assert vals.tolist() == [3.0, 3.0, 3.0, 2.0]
     y = np.array([-1.0, -1.0, -1.0], dtype=np.float32)
     assert omarg.top_k(y, 2)[0].tolist() == [0, 1]
+
+
+def check_hand_margins():
+    """Stop margins and cross-depth gaps of the hand-worked round, with their depth spans."""
+    g = _hand()
+    with open(os.path.join(HERE, "golden", "hand_example_margins.json")) as f:
+        gm = json.load(f)
+    logits = np.log(np.array(g["q"], dtype=np.float64)).astype(np.float32)
+    for case in gm["cases"]:
+        cap = case["cap"]
+        r = oracle.build_round(logits, "f32", g["K"], g["t_draft"], _costs_linear(cap, g["t_verify_slope"]), cap)
+        m = oracle.decision_margins(r.exp)
+        assert [sp for _, sp in m.stop] == [sp for _, sp in case["stop"]], (cap, m.stop)
+        np.testing.assert_allclose([v for v, _ in m.stop], [v for v, _ in case["stop"]], rtol=2e-6)
+        got = sorted(m.cross)
+        want = sorted(tuple(c) for c in case["cross"])
+        assert [sp for _, sp in got] == [sp for _, sp in want], (cap, got)
+        np.testing.assert_allclose([v for v, _ in got], [v for v, _ in want], rtol=0, atol=1e-6)
 
 
 def check_tie_stops():
@@ -277,6 +297,33 @@ def test_ties_stop():
     check_tie_stops()
 
 
+def test_hand_margins():
+    check_hand_margins()
+
+
+def test_guard_threshold_grows_with_depth_span():
+    from tests import _guard
+    M = oracle.Margins
+    assert _guard.required(1) == _guard.TAU
+    assert _guard.required(30) == 2 * 30 * _guard.LSE_ATOL > _guard.TAU
+    assert _guard.clears(M(stop=[(2e-6, 3)], cross=[(1.5e-6, 2)]))
+    # a gap of 3e-6 between depths 1 and 19 may flip under 18 normaliser errors of 1e-7 each
+    assert not _guard.clears(M(stop=[], cross=[(3e-6, 18)]))
+    assert not _guard.clears(M(stop=[(3e-6, 19)], cross=[]))
+    assert not _guard.clears(M(stop=[(9e-7, 1)], cross=[]))
+
+
+def test_margins_of_deep_rounds_carry_their_depth():
+    """Every stop margin's span is at least the tested node's depth, and every cross-depth gap is
+    non-negative (a frontier node never precedes a selected one)."""
+    x = _tiny_round(27, 6, 2, 5, scale=0.3)
+    nn = np.arange(64, dtype=np.float64)
+    r = oracle.build_round(x, "f32", 2, 1.0, 1.0 + 0.001 * nn, 63)
+    m = oracle.decision_margins(r.exp)
+    assert max(sp for _, sp in m.stop) == max(s.depth for s in r.exp.steps) >= 3
+    assert all(v >= 0 for v, _ in m.cross) and all(sp >= 1 for _, sp in m.cross)
+
+
 def test_flat_cost_region_always_expands():
     # zero marginal cost makes theta rise strictly, so the tree reaches the end of the flat region
     x = _tiny_round(25, 4, 3, 8)
@@ -390,16 +437,27 @@ MUTATIONS = [
     ("oracle.alg1", "kept = not (theta_new <= theta_prev)", "kept = not (theta_new < theta_prev)", check_tie_stops, ()),
     ("oracle.alg1", "A[d] = A[d - 1] + float(lse[d - 1])", "A[d] = A[d - 1] + float(lse[d % len(lse)])",
      check_top_n_bruteforce, (1, 3, 2, 5)),
-    ("oracle.alg1", "sig = min(lam - float(A[d]), base_sig)", "sig = min(lam + float(A[d]), base_sig)",
+    ("oracle.alg1", "sig = min(lam - float(self.A[d]), base_sig)", "sig = min(lam + float(self.A[d]), base_sig)",
      check_top_n_bruteforce, (1, 3, 2, 5)),
-    ("oracle.alg1", "if r + 1 < K:", "if r + 1 < K - 1:", check_top_n_bruteforce, (2, 2, 3, 5)),
-    ("oracle.alg1", "if d < L:", "if d < L - 1:", check_top_n_bruteforce, (2, 3, 2, 5)),
-    ("oracle.alg1", "lam = base_lam + float(logit[d - 1, ranks[-1]])",
-     "lam = base_lam + float(logit[ranks[-1] % L, (d - 1) % K])", check_top_n_bruteforce, (3, 3, 3, 6)),
+    ("oracle.alg1", "for r in range(self.K):", "for r in range(self.K - 1):", check_top_n_bruteforce, (2, 2, 3, 5)),
+    ("oracle.alg1", "if len(prefix) == self.L:", "if len(prefix) == self.L - 1:", check_top_n_bruteforce, (2, 3, 2, 5)),
+    ("oracle.alg1", "lam = base_lam + float(self.logit[d - 1, ranks[-1]])",
+     "lam = base_lam + float(self.logit[ranks[-1] % self.L, (d - 1) % self.K])", check_top_n_bruteforce, (3, 3, 3, 6)),
+    ("oracle.alg1", "order = sorted(listed, key=Node.key)", "order = sorted(listed, key=lambda nd: (nd.depth, nd.ranks))",
+     check_top_n_bruteforce, (1, 3, 2, 5)),
+    ("oracle.alg1", "if child.sigma < tau:", "if child.sigma < tau and r > 0:", check_top_n_bruteforce, (1, 3, 2, 5)),
+    ("oracle.alg1", "complete = len(listed) == tree.total", "complete = True", check_top_n_bruteforce, (1, 3, 2, 5)),
     ("oracle.alg1", "theta_new = (1.0 + phi + delta) / C(n + 1)", "theta_new = (phi + delta) / C(n + 1)",
      check_hand_example, ()),
     ("oracle.alg1", "theta_new = (1.0 + phi + delta) / C(n + 1)", "theta_new = (1.0 + phi + delta) / C(n)",
      check_hand_example, ()),
+    ("oracle.alg1", "if nd.depth < tree.L:", "if nd.depth < tree.L - 1:", check_hand_margins, ()),
+    ("oracle.alg1", "if r + 1 < tree.K:", "if r + 1 < tree.K - 1:", check_hand_margins, ()),
+    ("oracle.pipeline", "a = s.delta * s.c_n", "a = s.delta * s.c_next", check_hand_margins, ()),
+    ("oracle.pipeline", "b = (1.0 + s.phi) * c", "b = s.phi * c", check_hand_margins, ()),
+    ("oracle.pipeline", "stop.append((abs(a - b) / (abs(a) + abs(b)), max(s.depth, deepest)))",
+     "stop.append((abs(a - b) / (abs(a) + abs(b)), s.depth))", check_hand_margins, ()),
+    ("oracle.pipeline", "if d2 != d:", "if True:", check_hand_margins, ()),
     ("oracle.layout", "key=lambda i: (len(ranks[i]), ranks[i])", "key=lambda i: i", check_hand_example, ()),
     ("oracle.layout", "return TreeOut(rk, tok, par, dep, prob, pos_offset + dep)",
      "return TreeOut(rk, tok, par, dep, prob, pos_offset + dep - 1)", check_hand_example, ()),
