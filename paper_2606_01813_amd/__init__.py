@@ -48,6 +48,30 @@ def _stream(stream, device) -> int:
     return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
 
 
+def _on_device(t, device: int) -> bool:
+    return bool(t.is_cuda) and t.device.index == device
+
+
+def _check(name: str, t, dtype, dims, B: int, device: int, required: bool = True) -> None:
+    """Raises unless ``t`` is a contiguous tensor of ``dtype`` on cuda:``device`` shaped [>= B, *dims]."""
+    torch = _torch()
+    if t is None:
+        if required:
+            raise ValueError(f"{name} is required")
+        return
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor, got {type(t).__name__}")
+    if not _on_device(t, device):
+        raise ValueError(f"{name} must be on cuda:{device} (the plan's device), got {t.device}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != 1 + len(dims) or t.shape[0] < B or tuple(t.shape[1:]) != tuple(dims):
+        raise ValueError(f"{name} must have shape [>= {B}{''.join(', ' + str(d) for d in dims)}], "
+                         f"got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
 def fit_cost(x, y, cap: Optional[int] = None):
     """Convex non-decreasing least-squares fit of a cost profile (host, ``caddtree_fit_cost``).
 
@@ -123,6 +147,7 @@ class Plan:
         h = ctypes.c_void_p()
         _lib.check(self._lib.caddtree_plan_create(ctypes.byref(cfg), ctypes.byref(h)))
         self._h = h
+        self.device = _torch().cuda.current_device()   # the library binds the plan to this device
 
     # ------------------------------------------------------------ lifetime
     def close(self) -> None:
@@ -176,9 +201,14 @@ class Plan:
         return out
 
     # ------------------------------------------------------------ calls
+    # ------------------------------------------------------------ argument checks (before any C call)
     def _logits(self, logits):
         torch = _torch()
         want = torch.bfloat16 if self.dtype == "bf16" else torch.float32
+        if not isinstance(logits, torch.Tensor):
+            raise TypeError(f"logits must be a torch tensor, got {type(logits).__name__}")
+        if not _on_device(logits, self.device):
+            raise ValueError(f"logits must be on cuda:{self.device} (the plan's device), got {logits.device}")
         if logits.dtype != want:
             raise TypeError(f"logits must be {want}, got {logits.dtype}")
         if logits.dim() != 3 or logits.shape[1] != self.L or logits.shape[2] < self.V:
@@ -201,30 +231,75 @@ class Plan:
         if ctx_len is None:
             return None
         torch = _torch()
-        if ctx_len.dtype != torch.int64 or tuple(ctx_len.shape) != (B,) or not ctx_len.is_contiguous():
-            raise ValueError(f"ctx_len must be a contiguous int64 tensor of shape ({B},)")
+        _check("ctx_len", ctx_len, torch.int64, (), B, self.device)
+        if ctx_len.shape[0] != B:
+            raise ValueError(f"ctx_len must have shape ({B},), got {tuple(ctx_len.shape)}")
         return _ptr(ctx_len)
+
+    def _topk(self, B: int, ids, logit, lse, lq=None, required: bool = True) -> None:
+        torch = _torch()
+        _check("topk_ids", ids, torch.int32, (self.L, self.K), B, self.device, required)
+        _check("topk_logit", logit, torch.float32, (self.L, self.K), B, self.device, required)
+        _check("lse", lse, torch.float64, (self.L,), B, self.device, required)
+        _check("topk_lq", lq, torch.float32, (self.L, self.K), B, self.device, required=False)
+
+    def _tree(self, B: int, out: "TreeOutputs", emit: bool = False) -> None:
+        torch = _torch()
+        cap = max(self.cap, 1)
+        _check("parent", out.parent, torch.int32, (cap,), B, self.device)
+        _check("n_star", out.n_star, torch.int32, (), B, self.device)
+        _check("depth", out.depth, torch.int32, (cap,), B, self.device, required=not emit or out.pos_ids is not None)
+        if not emit:
+            _check("token_ids", out.token_ids, torch.int32, (cap,), B, self.device)
+            _check("path_prob", out.path_prob, torch.float32, (cap,), B, self.device, required=False)
+            _check("phi", out.phi, torch.float32, (), B, self.device, required=False)
+            _check("theta", out.theta, torch.float32, (), B, self.device, required=False)
+        else:
+            _check("pos_ids", out.pos_ids, torch.int32, (cap,), B, self.device, required=False)
+            if self.mask == "u8":
+                _check("mask", out.mask, torch.uint8, (cap, cap), B, self.device, required=False)
+            elif self.mask == "bits" and out.mask is not None:
+                if out.mask.dtype not in (torch.int32, getattr(torch, "uint32", torch.int32)):
+                    raise TypeError(f"mask must be int32 or uint32 words, got {out.mask.dtype}")
+                _check("mask", out.mask, out.mask.dtype, (cap, (cap + 31) // 32), B, self.device)
+
+    def _workspace(self, B: int, workspace, out: "TreeOutputs"):
+        torch = _torch()
+        if workspace is None:
+            return None, 0
+        if not isinstance(workspace, torch.Tensor) or not _on_device(workspace, self.device) \
+                or not workspace.is_contiguous():
+            raise ValueError(f"workspace must be a contiguous tensor on cuda:{self.device}")
+        return _ptr(workspace), workspace.numel() * workspace.element_size()
 
     def build(self, logits, out: TreeOutputs, pos_offset: int = 0, workspace=None, stream=None,
               ctx_len=None) -> None:
         B, stride = self._logits(logits)
-        ws_ptr = _ptr(workspace)
-        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        self._tree(B, out)
+        self._tree(B, out, emit=True)
+        self._topk(B, out.topk_ids, out.topk_logit, out.lse, out.topk_lq, required=False)
+        ws_ptr, ws_bytes = self._workspace(B, workspace, out)
+        ctx = self._ctx(ctx_len, B)
         st = out.as_struct()
         _lib.check(self._lib.caddtree_build(self._h, _ptr(logits), B, stride, int(pos_offset),
-                                            self._ctx(ctx_len, B), ctypes.byref(st), ws_ptr, ws_bytes,
+                                            ctx, ctypes.byref(st), ws_ptr, ws_bytes,
                                             _stream(stream, logits.device)))
 
     def reduce_topk(self, logits, topk_ids, topk_logit, lse, topk_lq=None, stream=None) -> None:
         B, stride = self._logits(logits)
+        self._topk(B, topk_ids, topk_logit, lse, topk_lq)
         _lib.check(self._lib.caddtree_reduce_topk(self._h, _ptr(logits), B, stride, _ptr(topk_ids),
                                                   _ptr(topk_logit), _ptr(topk_lq), _ptr(lse),
                                                   _stream(stream, logits.device)))
 
     def expand(self, topk_ids, topk_logit, lse, out: TreeOutputs, stream=None, ctx_len=None) -> None:
+        self._topk(0, topk_ids, topk_logit, lse)
         B = int(topk_ids.shape[0])
+        self._topk(B, topk_ids, topk_logit, lse)
+        self._tree(B, out)
+        ctx = self._ctx(ctx_len, B)
         _lib.check(self._lib.caddtree_expand(self._h, _ptr(topk_ids), _ptr(topk_logit), _ptr(lse), B,
-                                             self._ctx(ctx_len, B), _ptr(out.token_ids), _ptr(out.parent), _ptr(out.depth),
+                                             ctx, _ptr(out.token_ids), _ptr(out.parent), _ptr(out.depth),
                                              _ptr(out.path_prob), _ptr(out.n_star), _ptr(out.phi),
                                              _ptr(out.theta), _stream(stream, topk_ids.device)))
 
@@ -234,17 +309,28 @@ class Plan:
         drawn from the uniforms ``u`` (float64 [B, L]); writes ``accept_len`` (int32 [B]) and optionally
         ``round_cost`` (float64 [B], this plan's C_d + C_v(n*))."""
         torch = _torch()
-        B = int(tree.token_ids.shape[0])
-        if u.dtype != torch.float64 or tuple(u.shape) != (B, self.L) or not u.is_contiguous():
+        _check("token_ids", tree.token_ids, torch.int32, tree.token_ids.shape[1:] if tree.token_ids is not None
+               else (), 0, self.device)
+        B, stride = int(tree.token_ids.shape[0]), int(tree.token_ids.shape[1])
+        _check("parent", tree.parent, torch.int32, (stride,), B, self.device)
+        _check("n_star", tree.n_star, torch.int32, (), B, self.device)
+        self._topk(B, topk.topk_ids, topk.topk_logit, topk.lse)
+        _check("u", u, torch.float64, (self.L,), B, self.device)
+        if u.shape[0] != B:
             raise ValueError(f"u must be a contiguous float64 tensor of shape ({B}, {self.L})")
+        _check("accept_len", accept_len, torch.int32, (), B, self.device)
+        _check("round_cost", round_cost, torch.float64, (), B, self.device, required=False)
+        ctx = self._ctx(ctx_len, B) if round_cost is not None else None
         _lib.check(self._lib.caddtree_accept(self._h, _ptr(topk.topk_ids), _ptr(topk.topk_logit), _ptr(topk.lse),
                                              B, _ptr(tree.token_ids), _ptr(tree.parent),
-                                             int(tree.token_ids.shape[1]), _ptr(tree.n_star), _ptr(u),
-                                             self._ctx(ctx_len, B), _ptr(accept_len), _ptr(round_cost),
+                                             stride, _ptr(tree.n_star), _ptr(u),
+                                             ctx, _ptr(accept_len), _ptr(round_cost),
                                              _stream(stream, u.device)))
 
     def emit(self, out: TreeOutputs, pos_offset: int = 0, stream=None) -> None:
+        _check("parent", out.parent, _torch().int32, (max(self.cap, 1),), 0, self.device)
         B = int(out.parent.shape[0])
+        self._tree(B, out, emit=True)
         _lib.check(self._lib.caddtree_emit(self._h, _ptr(out.parent), _ptr(out.depth), _ptr(out.n_star), B,
                                            int(pos_offset), _ptr(out.mask), _ptr(out.pos_ids),
                                            _stream(stream, out.parent.device)))
