@@ -124,8 +124,12 @@ def cpu_baseline(cfg, xs, target_s: float, max_rounds: int):
     _POOL_XS, _POOL_CFG = xs, cfg
     t0 = time.perf_counter()
     deadline = time.time() + target_s
-    with mp.get_context("fork").Pool(workers) as pool:
+    pool = mp.get_context("fork").Pool(workers)
+    try:
         counts = pool.map(_pool_worker, [(w, workers, deadline) for w in range(workers)])
+    finally:
+        pool.close()
+        pool.join()
     dt = time.perf_counter() - t0
     _POOL_XS = None
     n = sum(counts)

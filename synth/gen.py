@@ -134,9 +134,12 @@ def draw_batch(cfg: Config, rounds: Optional[Sequence[int]] = None,
     shm = shared_memory.SharedMemory(create=True, size=max(1, out.nbytes))
     try:
         chunks = [work[k::workers] for k in range(workers)]
-        ctx = mp.get_context("spawn")
-        with ctx.Pool(workers, initializer=_worker_init, initargs=(shm.name,)) as pool:
+        pool = mp.get_context("spawn").Pool(workers, initializer=_worker_init, initargs=(shm.name,))
+        try:
             done = sum(pool.map(_worker_fill, [(sub, c) for c in chunks]))
+        finally:
+            pool.close()        # the workers exit on their own (no SIGTERM from terminate())
+            pool.join()
         assert done == n
         view = np.ndarray(shape, dtype=dt, buffer=shm.buf)
         out[...] = view
@@ -147,7 +150,17 @@ def draw_batch(cfg: Config, rounds: Optional[Sequence[int]] = None,
     return out
 
 
+def under_profiler() -> bool:
+    """True inside a rocprofv3 run: its launcher exports ROCPROF* variables, and a child process
+    would start the profiler (and, with counters, the GPU) again."""
+    return any(k.startswith("ROCPROF") for k in os.environ)
+
+
 def default_workers() -> int:
+    """Generator processes: every core this process may use, at most 16 (the host share of one GPU);
+    one (generate in this process) under the profiler."""
+    if under_profiler():
+        return 1
     try:
         n = len(os.sched_getaffinity(0))
     except AttributeError:  # pragma: no cover
