@@ -167,6 +167,27 @@ caddtree_status_t caddtree_build(caddtree_plan_t plan, const void* logits, int64
                                  int32_t pos_offset, const int64_t* ctx_len, const caddtree_outputs_t* out,
                                  void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): caddtree_build with no
+ * workspace argument.  The top-K table the caller does not ask for lives in a
+ * device array inside the library, CADDTREE_NOALLOC_SCRATCH_BYTES per GPU, held
+ * until the process ends; the call allocates and frees nothing and runs the same
+ * kernels as caddtree_build, with the same results.
+ *   Limit: caddtree_workspace_bytes(plan, B) for the top-K outputs left NULL
+ *   must not exceed CADDTREE_NOALLOC_SCRATCH_BYTES (8 MiB: about
+ *   2^20 / (L K + L) rounds, 7281 at L = 16, K = 8), else CADDTREE_E_WORKSPACE
+ *   and nothing is enqueued.  Passing every top-K output lifts the limit.
+ *   Every call on one GPU shares that GPU's array, whatever the plan or stream:
+ *   calls that overlap in time on one GPU race (serialise them, e.g. on one
+ *   stream).  Each call writes the part it reads before reading it, so nothing
+ *   needs clearing between calls.
+ *   Other arguments and errors as for caddtree_build; E_HIP if the array's
+ *   address could not be taken when the plan was created. */
+#define CADDTREE_NOALLOC_SCRATCH_BYTES ((size_t)8 << 20)
+caddtree_status_t caddtree_build_noalloc(caddtree_plan_t plan, const void* logits, int64_t B, int64_t row_stride,
+                                         int32_t pos_offset, const int64_t* ctx_len, const caddtree_outputs_t* out,
+                                         hipStream_t stream);
+
 /* Stage 1 (Sec. 3.2): per (round, position) row, LSE in fp64 and the top-K by
  * (value desc, id asc).  topk_ids, topk_logit, lse required; topk_lq optional. */
 caddtree_status_t caddtree_reduce_topk(caddtree_plan_t plan, const void* logits, int64_t B, int64_t row_stride,

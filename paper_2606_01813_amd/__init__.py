@@ -285,6 +285,19 @@ class Plan:
                                             ctx, ctypes.byref(st), ws_ptr, ws_bytes,
                                             _stream(stream, logits.device)))
 
+    def build_noalloc(self, logits, out: TreeOutputs, pos_offset: int = 0, stream=None, ctx_len=None) -> None:
+        """``build`` without a workspace (``caddtree_build_noalloc``): the top-K table not asked for in
+        ``out`` lives in the library's own device array, shared by every such call on the GPU, so calls
+        that overlap in time on one GPU race."""
+        B, stride = self._logits(logits)
+        self._tree(B, out)
+        self._tree(B, out, emit=True)
+        self._topk(B, out.topk_ids, out.topk_logit, out.lse, out.topk_lq, required=False)
+        ctx = self._ctx(ctx_len, B)
+        st = out.as_struct()
+        _lib.check(self._lib.caddtree_build_noalloc(self._h, _ptr(logits), B, stride, int(pos_offset), ctx,
+                                                    ctypes.byref(st), _stream(stream, logits.device)))
+
     def reduce_topk(self, logits, topk_ids, topk_logit, lse, topk_lq=None, stream=None) -> None:
         B, stride = self._logits(logits)
         self._topk(B, topk_ids, topk_logit, lse, topk_lq)

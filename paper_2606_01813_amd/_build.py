@@ -17,7 +17,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libcaddtree.so")
-SOURCES = ["api.cpp", "reduce_topk.hip", "expand.hip", "expand_level.hip", "emit.hip", "accept.hip", "costfit.cpp"]
+SOURCES = ["api.cpp", "reduce_topk.hip", "expand.hip", "expand_level.hip", "emit.hip", "accept.hip", "scratch.hip",
+           "costfit.cpp"]
 ARCH = os.environ.get("CADDTREE_ARCH", "gfx950")
 
 

@@ -14,6 +14,7 @@ MASKS = {"none": 0, "u8": 1, "bits": 2}
 ALLOW_NONCONVEX = 1
 FIXED_BUDGET = 2
 MAX_L, MAX_K, MAX_CAP, MAX_CTX = 32, 16, 4096, 64
+NOALLOC_SCRATCH_BYTES = 8 << 20
 
 
 class CaddtreeError(RuntimeError):
@@ -46,6 +47,7 @@ class Outputs(ctypes.Structure):
 
 EXPORTS = [
     "caddtree_plan_create", "caddtree_plan_destroy", "caddtree_workspace_bytes", "caddtree_build",
+    "caddtree_build_noalloc",
     "caddtree_reduce_topk", "caddtree_expand", "caddtree_emit", "caddtree_accept", "caddtree_fit_cost", "caddtree_status_string",
     "caddtree_last_error",
 ]
@@ -71,6 +73,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.caddtree_workspace_bytes.restype = sz
     lib.caddtree_build.argtypes = [vp, vp, i64, i64, i32, vp, ctypes.POINTER(Outputs), vp, sz, vp]
     lib.caddtree_build.restype = ctypes.c_int
+    lib.caddtree_build_noalloc.argtypes = [vp, vp, i64, i64, i32, vp, ctypes.POINTER(Outputs), vp]
+    lib.caddtree_build_noalloc.restype = ctypes.c_int
     lib.caddtree_reduce_topk.argtypes = [vp, vp, i64, i64, vp, vp, vp, vp, vp]
     lib.caddtree_reduce_topk.restype = ctypes.c_int
     lib.caddtree_expand.argtypes = [vp, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp]

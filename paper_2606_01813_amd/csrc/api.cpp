@@ -30,6 +30,7 @@ struct caddtree_plan {
   int device;
   int k1_waves;         // 0 = automatic
   int k1_unroll;        // 0 = automatic
+  bool noalloc_ready;   // the scratch array of caddtree_build_noalloc has an address on this device
 };
 
 namespace {
@@ -318,6 +319,9 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
     if (e == hipSuccess)
       e = hipMemcpy(p->d_ctx_grid, cfg->ctx_grid_host, sizeof(int64_t) * (size_t)J, hipMemcpyHostToDevice);
   }
+  // the no-allocation entry point's scratch array: its address on this device, taken once per device
+  p->noalloc_ready = caddtree::noalloc_scratch_init(p->device) == hipSuccess;
+  (void)hipGetLastError();
   if (e == hipSuccess) e = caddtree::expand_prepare(p->L, p->K, p->cap);
   if (e == hipSuccess) e = caddtree::expand_level_prepare();
   if (e != hipSuccess) {
@@ -392,28 +396,35 @@ caddtree_status_t caddtree_emit(caddtree_plan_t p, const int32_t* parent, const 
   return ok();
 }
 
-caddtree_status_t caddtree_build(caddtree_plan_t p, const void* logits, int64_t B, int64_t row_stride,
-                                 int32_t pos_offset, const int64_t* ctx_len, const caddtree_outputs_t* out,
-                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Argument checks shared by caddtree_build and caddtree_build_noalloc; *done is set when B = 0.
+caddtree_status_t check_build(const caddtree_plan* p, const void* logits, int64_t B, int64_t row_stride,
+                              const int64_t* ctx_len, const caddtree_outputs_t* out, bool* done) {
+  *done = false;
   caddtree_status_t st = check_plan(p);
   if (st != CADDTREE_OK) return st;
   if ((st = check_logits(p, logits, B, row_stride)) != CADDTREE_OK) return st;
   if (out == nullptr) return fail(CADDTREE_E_INVALID, "out is NULL");
-  if (B == 0) return ok();
+  if (B == 0) {
+    *done = true;
+    return CADDTREE_OK;
+  }
   if (out->token_ids == nullptr || out->parent == nullptr || out->depth == nullptr || out->n_star == nullptr)
     return fail(CADDTREE_E_INVALID, "out->token_ids, parent, depth and n_star are required");
   if (B > (int64_t)INT32_MAX) return fail(CADDTREE_E_UNSUPPORTED, "B exceeds 2^31 - 1");
-  if ((st = check_ctx(p, ctx_len)) != CADDTREE_OK) return st;
+  return check_ctx(p, ctx_len);
+}
+
+// The three stages on `stream`, the top-K table the caller did not ask for carved from `workspace`.
+caddtree_status_t run_build(const caddtree_plan* p, const void* logits, int64_t B, int64_t row_stride,
+                            int32_t pos_offset, const int64_t* ctx_len, const caddtree_outputs_t* out,
+                            void* workspace, hipStream_t stream) {
   TopkBuffers tb;
-  const size_t need = topk_workspace(p, B, out, nullptr, &tb);
-  if (need > 0) {
-    if (workspace == nullptr) return fail(CADDTREE_E_WORKSPACE, "workspace is NULL, %zu bytes needed", need);
-    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
-      return fail(CADDTREE_E_WORKSPACE, "workspace must be 256-byte aligned");
-    if (workspace_bytes < need)
-      return fail(CADDTREE_E_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, need);
-  }
   topk_workspace(p, B, out, static_cast<char*>(workspace), &tb);
+  caddtree_status_t st;
   if ((st = run_reduce(p, logits, B, row_stride, tb.ids, tb.logit, out->topk_lq, tb.lse, stream)) != CADDTREE_OK)
     return st;
   if ((st = run_expand(p, tb.ids, tb.logit, tb.lse, B, ctx_len, out->token_ids, out->parent, out->depth,
@@ -423,6 +434,51 @@ caddtree_status_t caddtree_build(caddtree_plan_t p, const void* logits, int64_t 
       CADDTREE_OK)
     return st;
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+caddtree_status_t caddtree_build(caddtree_plan_t p, const void* logits, int64_t B, int64_t row_stride,
+                                 int32_t pos_offset, const int64_t* ctx_len, const caddtree_outputs_t* out,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  bool done;
+  caddtree_status_t st = check_build(p, logits, B, row_stride, ctx_len, out, &done);
+  if (st != CADDTREE_OK) return st;
+  if (done) return ok();
+  TopkBuffers tb;
+  const size_t need = topk_workspace(p, B, out, nullptr, &tb);
+  if (need > 0) {
+    if (workspace == nullptr) return fail(CADDTREE_E_WORKSPACE, "workspace is NULL, %zu bytes needed", need);
+    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+      return fail(CADDTREE_E_WORKSPACE, "workspace must be 256-byte aligned");
+    if (workspace_bytes < need)
+      return fail(CADDTREE_E_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, need);
+  }
+  return run_build(p, logits, B, row_stride, pos_offset, ctx_len, out, workspace, stream);
+}
+
+caddtree_status_t caddtree_build_noalloc(caddtree_plan_t p, const void* logits, int64_t B, int64_t row_stride,
+                                         int32_t pos_offset, const int64_t* ctx_len, const caddtree_outputs_t* out,
+                                         hipStream_t stream) {
+  bool done;
+  caddtree_status_t st = check_build(p, logits, B, row_stride, ctx_len, out, &done);
+  if (st != CADDTREE_OK) return st;
+  if (done) return ok();
+  TopkBuffers tb;
+  const size_t need = topk_workspace(p, B, out, nullptr, &tb);
+  void* scratch = nullptr;
+  if (need > 0) {
+    if (need > caddtree::kNoAllocScratchBytes)
+      return fail(CADDTREE_E_WORKSPACE,
+                  "the top-K table of %lld rounds needs %zu bytes, beyond the %zu-byte library scratch; pass the "
+                  "top-K outputs or use caddtree_build with a workspace",
+                  (long long)B, need, caddtree::kNoAllocScratchBytes);
+    if (!p->noalloc_ready || (scratch = caddtree::noalloc_scratch(p->device)) == nullptr)
+      return fail(CADDTREE_E_HIP, "the library scratch has no address on device %d", p->device);
+  }
+  return run_build(p, logits, B, row_stride, pos_offset, ctx_len, out, scratch, stream);
 }
 
 caddtree_status_t caddtree_accept(caddtree_plan_t p, const int32_t* topk_ids, const float* topk_logit,

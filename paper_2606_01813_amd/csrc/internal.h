@@ -100,6 +100,13 @@ struct AcceptArgs {
 };
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t stream);
 
+// Library-owned scratch for caddtree_build_noalloc (scratch.hip): one array per GPU of this many
+// bytes.  noalloc_scratch_init takes its address on `device`, which must be current, once per device;
+// noalloc_scratch returns that address (nullptr before a successful init).
+constexpr size_t kNoAllocScratchBytes = CADDTREE_NOALLOC_SCRATCH_BYTES;
+hipError_t noalloc_scratch_init(int device);
+void* noalloc_scratch(int device);
+
 // Host: convex non-decreasing least-squares fit of a cost profile (costfit.cpp); false if the
 // active-set iteration did not settle.
 bool fit_convex_cost(const double* x_host, const double* y_host, int n, double* fit_host, int32_t cap,
