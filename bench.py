@@ -72,11 +72,14 @@ _POOL_XS = None     # the batch, shared with forked workers (copy-on-write)
 _POOL_CFG = None
 
 
-def _oracle_round(cfg, x, b: int, tv_plain, ctx):
+def _oracle_round(cfg, x, b: int, tv_plain, ctx) -> bool:
+    """One round through the oracle; True if its decision margins clear the parity tests' input guard."""
     import oracle
+    from tests._guard import clears
     tv = tv_plain if ctx is None else oracle.context_cost(ctx[1], ctx[0], int(ctx[2][b]))
-    oracle.build_round(x, cfg.dtype, cfg.K, cfg.t_draft, tv, cfg.cap, mask=cfg.mask,
-                       budget=cfg.cap if cfg.fixed else None)
+    r = oracle.build_round(x, cfg.dtype, cfg.K, cfg.t_draft, tv, cfg.cap, mask=cfg.mask,
+                           budget=cfg.cap if cfg.fixed else None)
+    return clears(oracle.decision_margins(r.exp))
 
 
 def _pool_worker(args):
@@ -87,13 +90,13 @@ def _pool_worker(args):
     if cfg.ctx:
         grid, tables = synth.ctx_tables(cfg)
         ctx = (grid, tables, synth.ctx_lengths(cfg, cfg.B))
-    n = 0
+    n = near = 0
     b = start
     while b < xs.shape[0] and time.time() < deadline:
-        _oracle_round(cfg, xs[b], b, tv, ctx)
+        near += not _oracle_round(cfg, xs[b], b, tv, ctx)
         n += 1
         b += stride
-    return n
+    return n, near
 
 
 def cpu_baseline(cfg, xs, target_s: float, max_rounds: int):
@@ -132,9 +135,13 @@ def cpu_baseline(cfg, xs, target_s: float, max_rounds: int):
         pool.join()
     dt = time.perf_counter() - t0
     _POOL_XS = None
-    n = sum(counts)
+    n = sum(c[0] for c in counts)
+    near = sum(c[1] for c in counts)
     return {"value": n / dt, "unit": "rounds/s", "cores": workers, "kind": "oracle",
             "single_core_value": one,
+            "guard": {"rounds": n, "near_a_tie": near,
+                      "rule": "a round is near a tie when a stop margin or cross-depth gap is below "
+                              "max(1e-6, 2 * depth span * 1e-7); the parity tests redraw such rounds"},
             "sample": f"{n} rounds of {cfg.name} on a fork pool of {workers} workers ({dt:.1f} s; "
                       f"{avail} cores available), and {n1} rounds on one core; single-process fp64 numpy oracle "
                       f"(LSE + top-K + Algorithm 1 + mask per round); input generation excluded"}
@@ -154,6 +161,59 @@ def copy_probe(mib: int) -> None:
     torch.mul(x, 1.0, out=y)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4, "launches": 1}), flush=True)
+
+
+PROBE_LIB = os.path.join(ROOT, "paper_2606_01813_amd", "libcaddtree_probe.so")
+
+
+def read_probe(logits, cfg, stream, reps: int = 10):
+    """Best pure-read time over the logits batch (same rows, same 16-byte non-temporal loads as the
+    reduction kernel, no arithmetic), over every wave split and load depth: the bandwidth a read of this
+    shape reaches on this GPU.  None when the rows are not whole 16-byte units."""
+    import ctypes
+    import torch
+    es = cfg.elem_bytes
+    row_bytes = cfg.V * es
+    stride = int(logits.stride(1)) * es
+    if row_bytes % 16 or stride % 16 or logits.data_ptr() % 16:
+        return None
+    lib = ctypes.CDLL(PROBE_LIB)
+    lib.caddtree_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                        ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    lib.caddtree_probe_read.restype = ctypes.c_int
+    sink = torch.zeros(1, dtype=torch.int32, device=logits.device)
+    rows = cfg.B * cfg.L
+    best = None
+    for waves in (1, 2, 4, 8, 16):
+        for unroll in (4, 8):
+            def launch():
+                rc = lib.caddtree_probe_read(logits.data_ptr(), rows, stride, row_bytes, waves, unroll,
+                                             sink.data_ptr(), stream.cuda_stream)
+                if rc != 0:
+                    raise RuntimeError(f"read probe launch failed: hipError {rc}")
+            for _ in range(2):
+                launch()
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+            for a, b in ev:
+                a.record(stream)
+                launch()
+                b.record(stream)
+            torch.cuda.synchronize()
+            us = float(np.median([a.elapsed_time(b) for a, b in ev])) * 1e3
+            if best is None or us < best["us"]:
+                best = {"us": us, "waves_per_row": waves, "unroll": unroll}
+    best["bytes"] = rows * row_bytes
+    best["gbs"] = best["bytes"] / (best["us"] * 1e-6) / 1e9
+    return best
+
+
+def nstar_histogram(ns):
+    """Counts of n* in power-of-two bins [0, 1), [1, 2), [2, 4), .. (the last bin ends past the largest n*)."""
+    edges = [0, 1]
+    while edges[-1] <= int(ns.max()):
+        edges.append(edges[-1] * 2)
+    counts, _ = np.histogram(ns, bins=edges)
+    return {"edges": edges, "counts": counts.tolist()}
 
 
 DDTREE_GRID = (16, 32, 64, 128, 256, 512, 1024)
@@ -287,14 +347,19 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # timed region: K whole-path steps
+    # timed region: K whole-path steps, each bracketed by HIP events on the launch stream
+    step_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for a, b in step_ev:
+        a.record(stream)
         step()
+        b.record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    log(f"[bench] {args.steps} steps in {elapsed * 1e3:.2f} ms")
+    step_us = np.array([a.elapsed_time(b) for a, b in step_ev]) * 1e3
+    log(f"[bench] {args.steps} steps in {elapsed * 1e3:.2f} ms; median step {np.median(step_us):.1f} us")
 
     # per-stage durations (same work through the stage entry points), HIP events on the launch stream
     topk = plan.new_outputs(B, topk=True)
@@ -315,10 +380,16 @@ def main():
     ns = out.n_star.cpu().numpy()
     same = bool(torch.equal(out.n_star, topk.n_star) and torch.equal(out.token_ids, topk.token_ids))
 
+    probe = read_probe(logits, cfg, stream)
+    if probe:
+        log(f"[bench] read probe {probe['us']:.1f} us = {probe['gbs']:.0f} GB/s "
+            f"({probe['waves_per_row']} waves per row, {probe['unroll']} loads in flight)")
+
     rows = B * cfg.L
     k1_bytes = rows * cfg.V * cfg.elem_bytes + rows * (cfg.K * 12 + 8)
     achieved = k1_bytes / (k1.mean() * 1e-6) / 1e9
-    value = B * args.steps / elapsed
+    med_step = float(np.median(step_us))
+    value = B / (med_step * 1e-6)
     line = {
         "metric": METRIC,
         "value": value,
@@ -326,7 +397,8 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": elapsed * 1e3 / args.steps,
+        "ms_per_step": med_step * 1e-3,
+        "wall_ms_per_step": elapsed * 1e3 / args.steps,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -341,11 +413,18 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(cfg.name),
                      "kernel": "reduce_topk_kernel", "bytes_per_launch": k1_bytes,
-                     "avg_launch_us": float(k1.mean())},
+                     "avg_launch_us": float(k1.mean()),
+                     "probe_gbs": probe["gbs"] if probe else None,
+                     "pct_of_probe": achieved / probe["gbs"] if probe else None},
+        "read_probe": probe,
         "cpu_baseline": cpu,
         "stages_us": {"reduce_topk": float(k1.mean()), "expand": float(k2.mean()), "emit": float(k3.mean())},
-        "end_to_end_hbm_frac": (cfg.batch_bytes * args.steps / elapsed) / 1e9 / HBM_PEAK_GBS,
-        "n_star": {"mean": float(ns.mean()), "std": float(ns.std()), "min": int(ns.min()), "max": int(ns.max())},
+        "stages_median_us": {"reduce_topk": float(np.median(k1)), "expand": float(np.median(k2)),
+                             "emit": float(np.median(k3))},
+        "step_us": {"median": med_step, "min": float(step_us.min()), "max": float(step_us.max())},
+        "end_to_end_hbm_frac": cfg.batch_bytes / (med_step * 1e-6) / 1e9 / HBM_PEAK_GBS,
+        "n_star": {"mean": float(ns.mean()), "std": float(ns.std()), "min": int(ns.min()), "max": int(ns.max()),
+                   "histogram": nstar_histogram(ns)},
         "stage_path_matches_build": same,
     }
     print(json.dumps(line), flush=True)
