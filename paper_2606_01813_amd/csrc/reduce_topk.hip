@@ -18,7 +18,8 @@
 // (>= K) disjoint lane groups of the group maximum over the first chunks, which
 // is <= the K-th largest element, so no top-K element is ever filtered out.
 //
-// At the end, wave 0 merges the other waves' lists, combines the per-wave sums,
+// At the end, wave 0 merges the waves' lists (each candidate ranked against all of
+// them in one pass when they fit in one wave), combines the per-wave sums,
 // and replaces the top-K terms' fp32 exp2 values (recomputed bit-identically
 // from the exponent recorded at insertion) by fp64 values, which removes the
 // error of the largest terms from the normaliser.
@@ -227,11 +228,12 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
   int c = c0;
   if (kAligned) {
     const uint4* p4 = reinterpret_cast<const uint4*>(rowp);
-    // first group: reference exponent and the initial threshold
     if (c + kUnroll <= cfull) {
+      const uint4* lp = p4 + lane + (int64_t)c * (CH / VEC);   // chunk c of this lane
       uint4 q[kUnroll];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) q[u] = stream_load(p4 + ((c + u) * CH + lane * VEC) / VEC);
+      for (int u = 0; u < kUnroll; ++u) q[u] = stream_load(lp + u * (CH / VEC));
+      // the first group sets the reference exponent and the initial threshold
       float g = -INFINITY;
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {   // unpacked twice: keeps the live registers to one chunk
@@ -249,21 +251,8 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
       for (int o = 1; o < grp; o <<= 1) gm = fmaxf(gm, __shfl_xor(gm, o));
       for (int o = grp; o < kWave; o <<= 1) gm = fminf(gm, __shfl_xor(gm, o));
       s.thr = gm;
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        float x[VEC];
-        unpack(q[u], x);
-        chunk_full<VEC>(s, x, (c + u) * CH, K);
-      }
-      c += kUnroll;
-    }
-    // steady state: a ring of kUnroll loads in flight; each chunk's slot is refilled with the load
-    // kUnroll chunks ahead as soon as its registers are unpacked, before its arithmetic
-    if (c + kUnroll <= cfull) {
-      const uint4* lp = p4 + lane + (int64_t)c * (CH / VEC);   // chunk c of this lane
-      uint4 q[kUnroll];
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) q[u] = stream_load(lp + u * (CH / VEC));
+      // a ring of kUnroll loads in flight: each chunk's slot (the first group's too) is refilled with the
+      // load kUnroll chunks ahead as soon as its registers are unpacked, before its arithmetic
       for (; c + 2 * kUnroll <= cfull; c += kUnroll) {
         lp += kUnroll * (CH / VEC);
 #pragma unroll
@@ -301,22 +290,34 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
     chunk<VEC>(s, x, ok, c * CH, K);
   }
 
-  // wave sum of the per-lane accumulators (fixed order, deterministic)
-  double acc = s.acc;
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o);
+  // wave sum of the per-lane accumulators (fixed order: a DPP scan, the total in the last lane)
+  const double acc = xp::rl_d(xp::wave_incl_scan(s.acc), kWave - 1);
   if (lane < 16) { s_lv[wave][lane] = s.lv; s_lid[wave][lane] = s.lid; s_lr[wave][lane] = s.lr; }
   if (lane == 0) { s_acc[wave] = acc; s_r[wave] = s.r; }
   __syncthreads();
   if (wave != 0) return;
 
-  for (int w = 1; w < S; ++w) {
-    for (int k = 0; k < K; ++k) {
-      const float v = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(s_lv[w][k])));
-      const int id = __builtin_amdgcn_readfirstlane(s_lid[w][k]);
-      const float rr = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(s_lr[w][k])));
-      if (!before(v, id, s.thr, s.thr_id)) break;   // the rest of this sorted list cannot enter
-      list_insert(s, v, id, rr, K);
+  if (S * K <= kWave) {
+    // every wave's K best, one per lane: a lane's rank among them (ids are distinct) is its slot in
+    // the merged list; only slots below K are needed, and those hold real entries
+    const bool has = lane < S * K;
+    const int w = has ? lane / K : 0, k = has ? lane % K : 0;
+    const float v = has ? s_lv[w][k] : -INFINITY;
+    const int id = has ? s_lid[w][k] : INT_MAX;
+    const float rr = has ? s_lr[w][k] : 0.f;
+    int rank = 0;
+    for (int j = 0; j < S * K; ++j) rank += before(readlane_f(v, j), readlane_i(id, j), v, id) ? 1 : 0;
+    if (has && rank < K) { s_lv[0][rank] = v; s_lid[0][rank] = id; s_lr[0][rank] = rr; }
+    if (lane < K) { s.lv = s_lv[0][lane]; s.lid = s_lid[0][lane]; s.lr = s_lr[0][lane]; }
+  } else {
+    for (int w = 1; w < S; ++w) {
+      for (int k = 0; k < K; ++k) {
+        const float v = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(s_lv[w][k])));
+        const int id = __builtin_amdgcn_readfirstlane(s_lid[w][k]);
+        const float rr = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(s_lr[w][k])));
+        if (!before(v, id, s.thr, s.thr_id)) break;   // the rest of this sorted list cannot enter
+        list_insert(s, v, id, rr, K);
+      }
     }
   }
   float R = s_r[0];
@@ -329,8 +330,7 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
     const double exact = exp2((double)s.lv * kLog2eD - (double)R);
     corr = exact - approx;
   }
-#pragma unroll
-  for (int o = 8; o >= 1; o >>= 1) corr += __shfl_xor(corr, o);
+  corr = xp::rl_d(xp::wave_incl_scan(corr), kWave - 1);
   const double lse = (double)R * kLn2D + log(sum + corr);
   if (lane < K) {
     const int64_t o = row * K + lane;
