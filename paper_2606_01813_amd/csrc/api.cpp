@@ -31,6 +31,7 @@ struct caddtree_plan {
   int k1_waves;         // 0 = automatic
   int k1_unroll;        // 0 = automatic
   bool noalloc_ready;   // the scratch array of caddtree_build_noalloc has an address on this device
+  bool fuse_emit;       // caddtree_build lets the expansion's epilogue write the mask and position ids
 };
 
 namespace {
@@ -135,8 +136,9 @@ caddtree_status_t check_ctx(const caddtree_plan* p, const int64_t* ctx_len) {
 caddtree_status_t run_expand(const caddtree_plan* p, const int32_t* ids, const float* logit, const double* lse,
                              int64_t B, const int64_t* ctx_len, int32_t* token_ids, int32_t* parent,
                              int32_t* depth, float* path_prob, int32_t* n_star, float* phi, float* theta,
-                             hipStream_t stream) {
+                             hipStream_t stream, const caddtree::EmitOut* em = nullptr) {
   caddtree::ExpandArgs a;
+  a.em = em ? *em : caddtree::EmitOut{nullptr, nullptr, (int)CADDTREE_MASK_NONE, 0};
   a.topk_ids = ids;
   a.topk_logit = logit;
   a.lse = lse;
@@ -298,6 +300,14 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
   if (const char* env = std::getenv("CADDTREE_EXPAND")) {
     if (std::strcmp(env, "serial") == 0) p->use_level = false;
   }
+  // The expansion kernels can write each round's mask and position ids from the tree still in LDS,
+  // one wavefront per round, which saves a launch.  That pays for the trees a rising cost keeps small;
+  // fixed budgets and costs flat up to the cap (trees of the full cap) and long flat starts keep the
+  // emission kernel, whose many workgroups per round write large masks faster.
+  p->fuse_emit = !lean && flat_start < 512;
+  if (const char* env = std::getenv("CADDTREE_EMIT")) {
+    if (std::strcmp(env, "separate") == 0) p->fuse_emit = false;
+  }
   p->k1_waves = 0;
   if (const char* env = std::getenv("CADDTREE_K1_WAVES")) {
     const int w = std::atoi(env);
@@ -427,11 +437,15 @@ caddtree_status_t run_build(const caddtree_plan* p, const void* logits, int64_t 
   caddtree_status_t st;
   if ((st = run_reduce(p, logits, B, row_stride, tb.ids, tb.logit, out->topk_lq, tb.lse, stream)) != CADDTREE_OK)
     return st;
+  caddtree::EmitOut em{p->mask == CADDTREE_MASK_NONE ? nullptr : out->mask, out->pos_ids, (int)p->mask, pos_offset};
+  const bool fused = p->fuse_emit && p->cap > 0;
   if ((st = run_expand(p, tb.ids, tb.logit, tb.lse, B, ctx_len, out->token_ids, out->parent, out->depth,
-                       out->path_prob, out->n_star, out->phi, out->theta, stream)) != CADDTREE_OK)
-    return st;
-  if ((st = run_emit(p, out->parent, out->depth, out->n_star, B, pos_offset, out->mask, out->pos_ids, stream)) !=
+                       out->path_prob, out->n_star, out->phi, out->theta, stream, fused ? &em : nullptr)) !=
       CADDTREE_OK)
+    return st;
+  if (!fused &&
+      (st = run_emit(p, out->parent, out->depth, out->n_star, B, pos_offset, out->mask, out->pos_ids, stream)) !=
+          CADDTREE_OK)
     return st;
   return ok();
 }

@@ -44,7 +44,7 @@ hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream) {
     only_flagged = 1;
   }
   const serial::Args sa{a.topk_ids, a.topk_logit, a.lse, a.L, a.K, a.cap, a.cost, a.fixed_budget ? 1 : 0,
-                        a.token_ids, a.parent, a.depth, a.path_prob, a.n_star, a.phi, a.theta};
+                        a.token_ids, a.parent, a.depth, a.path_prob, a.n_star, a.phi, a.theta, a.em};
   hipLaunchKernelGGL(expand_kernel, dim3((unsigned)a.B), dim3(serial::kThreads), lds, stream, sa, only_flagged);
   return hipGetLastError();
 }

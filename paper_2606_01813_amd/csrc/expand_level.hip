@@ -697,7 +697,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
                     int flat, int setcap, int32_t* __restrict__ token_ids,
                     int32_t* __restrict__ parent_out, int32_t* __restrict__ depth_out,
                     float* __restrict__ path_prob, int32_t* __restrict__ n_star_out,
-                    float* __restrict__ phi_out, float* __restrict__ theta_out, int in_place) {
+                    float* __restrict__ phi_out, float* __restrict__ theta_out, int in_place, EmitOut em) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int b = blockIdx.x;
   const int lane = threadIdx.x;
@@ -769,7 +769,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       // flat for longer than the set holds: the serial form's case
       if (in_place)
         serial_in_place(serial::Args{topk_ids, topk_logit, lse, L, K, cap, ct, fixed, token_ids, parent_out,
-                                     depth_out, path_prob, n_star_out, phi_out, theta_out}, b);
+                                     depth_out, path_prob, n_star_out, phi_out, theta_out, em}, b);
       else if (lane == 0)
         n_star_out[b] = -1;
       return;
@@ -902,7 +902,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   if (!done) {                              // left to the serial form
     if (in_place)
       serial_in_place(serial::Args{topk_ids, topk_logit, lse, L, K, cap, ct, fixed, token_ids, parent_out,
-                                   depth_out, path_prob, n_star_out, phi_out, theta_out}, b);
+                                   depth_out, path_prob, n_star_out, phi_out, theta_out, em}, b);
     else if (lane == 0)
       n_star_out[b] = -1;
     return;
@@ -924,17 +924,24 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
     base += __popcll(m);
   }
   const int64_t ob = (int64_t)b * cap;
+  int16_t* par = reinterpret_cast<int16_t*>(s.dl);       // output parents, for the mask (dl is done)
   for (int i = lane; i < ns; i += kW) {
     const int o = s.pos[i];
     if (o >= 0) {
       const uint32_t m = s.meta[i];
       const int p = m_parent(m), d = m_depth(m), r = m_rank(m);
+      const int po = p < 0 ? -1 : (int)s.pos[p];
       token_ids[ob + o] = s.tid[(d - 1) * K + r];
-      parent_out[ob + o] = p < 0 ? -1 : (int)s.pos[p];
+      parent_out[ob + o] = po;
       depth_out[ob + o] = d;
       if (path_prob) path_prob[ob + o] = (float)exp(s.sl[i].x);
+      if (em.pos_ids) em.pos_ids[ob + o] = em.pos_offset + d;
+      par[o] = (int16_t)po;
     }
   }
+  __syncthreads();
+  // the mask, in the set's (sigma, Lambda) region (free now; emit_tile_bytes(n) <= 16 setcap bytes)
+  emit_mask_wave(par, n, cap, em.mask_kind, em.round_mask(b, cap), reinterpret_cast<uint32_t*>(s.sl), lane);
 }
 
 }  // namespace
@@ -965,7 +972,7 @@ hipError_t launch_expand_level(const ExpandArgs& a, size_t in_place_lds, hipStre
   hipLaunchKernelGGL(expand_level_kernel, dim3((unsigned)a.B), dim3(kW), lds, stream, a.topk_ids, a.topk_logit,
                      a.lse, a.L, a.K, a.cap, a.cost, a.fixed_budget ? 1 : 0, (!a.fixed_budget && a.flat_cost) ? 1 : 0,
                      a.level_set_cap, a.token_ids, a.parent, a.depth, a.path_prob, a.n_star, a.phi, a.theta,
-                     in_place_lds > 0 ? 1 : 0);
+                     in_place_lds > 0 ? 1 : 0, a.em);
   return hipGetLastError();
 }
 

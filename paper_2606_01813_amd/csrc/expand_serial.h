@@ -46,6 +46,7 @@
 #include <cmath>
 #include <type_traits>
 
+#include "emit_wave.h"
 #include "expand_common.h"
 
 namespace caddtree {
@@ -207,6 +208,7 @@ struct Args {
   int32_t* n_star_out;
   float* phi_out;
   float* theta_out;
+  EmitOut em;          // mask and position ids, when this epilogue writes them
 };
 
 // Round b, by the calling 64-lane workgroup, in the dynamic LDS (lds_bytes(L * K, cap) bytes).
@@ -468,15 +470,22 @@ __device__ __forceinline__ void expand_round(const Args& a, int b) {
   __syncthreads();
 
   const int64_t ob = (int64_t)b * cap;
+  int16_t* par = reinterpret_cast<int16_t*>(s.slam);     // output parents, for the mask (slam is done)
   for (int v = lane; v < n; v += kThreads) {
     const uint32_t m = s.smeta[v];
     const int p = m_parent(m), d = m_depth(m), r = m_rank(m);
     const int i = s.pos[v];
+    const int pi = p < 0 ? -1 : (int)s.pos[p];
     token_ids[ob + i] = s.tid[(d - 1) * K + r];
-    parent_out[ob + i] = p < 0 ? -1 : (int)s.pos[p];
+    parent_out[ob + i] = pi;
     depth_out[ob + i] = d;
     if (path_prob) path_prob[ob + i] = (float)exp(s.ssig[v]);
+    if (a.em.pos_ids) a.em.pos_ids[ob + i] = a.em.pos_offset + d;
+    par[i] = (int16_t)pi;
   }
+  __syncthreads();
+  // the mask, in the key/heap region (free now; it holds emit_tile_bytes(n) <= 16 cap bytes)
+  emit_mask_wave(par, n, cap, a.em.mask_kind, a.em.round_mask(b, cap), reinterpret_cast<uint32_t*>(s.key), lane);
 }
 
 }  // namespace serial

@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include "caddtree.h"
+#include "emit_wave.h"
 #include "expand_common.h"
 
 namespace caddtree {
@@ -51,6 +52,7 @@ struct ExpandArgs {
   int32_t level_set_cap;   // its threshold-set capacity
   bool fixed_budget;       // no stop rule: keep the top min(cap, #nodes) nodes (DDTree)
   bool flat_cost;          // every table holds one value: C(n) = C(0) up to the cap
+  EmitOut em;              // mask and position ids written by the expansion's epilogue (null: not here)
 };
 size_t expand_lds_bytes(int32_t L, int32_t K, int32_t cap);
 hipError_t expand_prepare(int32_t L, int32_t K, int32_t cap);  // raises the dynamic-LDS limit once

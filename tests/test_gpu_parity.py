@@ -194,6 +194,35 @@ def _paths_agree(outs):
             assert np.array_equal(v, outs["serial"][k]), k
 
 
+@pytest.mark.parametrize("name,kw", [
+    ("c1", dict(V=4000, B=8)),                           # dense mask, batched expansion
+    ("c1", dict(V=4000, B=8, mask="bits", L=9)),
+    ("c3", dict(V=4000, B=6)),                           # packed mask, flat start (n* >= 64: two row tiles)
+    ("s2", dict(V=1500, B=3)),                           # deep trees of 100-200 nodes
+    ("c4", dict(V=900, B=3, cost="tiny", cap=1500)),     # the serial form in place, trees past 64 rows
+    ("c4", dict(V=900, B=2, cost="tiny", cap=4096)),     # rounds flagged for the serial kernel
+    ("c0", dict(B=24, cap=7)),                           # cap below one mask word; trees cut by the cap
+])
+def test_fused_emit_matches_emit_kernel(name, kw, monkeypatch):
+    """caddtree_build's expansion epilogue writes the mask and position ids itself; they equal the
+    emission kernel's bit for bit (and the oracle's, on the guarded rounds)."""
+    cfg = synth.get_config(name).replace(**kw)
+    xs = synth.draw_batch(cfg)
+    lg = torch_logits(cfg, xs)
+    outs = {}
+    for mode in ("fused", "separate"):
+        if mode == "separate":
+            monkeypatch.setenv("CADDTREE_EMIT", "separate")
+        plan = make_plan(cfg)
+        outs[mode] = host(run_build(plan, lg, pos_offset=5))
+        plan.close()
+    a, b = outs["fused"], outs["separate"]
+    say(f"[emit] {cfg.name} L={cfg.L} K={cfg.K} cap={cfg.cap} mask={cfg.mask} n*={a['n_star'].tolist()[:8]}")
+    assert a["n_star"].max() > 0
+    for k in ("n_star", "token_ids", "parent", "depth", "pos_ids", "mask", "path_prob", "phi", "theta"):
+        assert np.array_equal(a[k], b[k]), f"{k} differs between the fused and the separate emission"
+
+
 def test_emit_stage_on_oracle_trees():
     import torch
     cfg = synth.get_config("s2").replace(V=1200, B=3)
