@@ -17,6 +17,7 @@
 // breadth-first node list from just past the current node (children follow
 // their parent in that order) with one ballot per 64 nodes.
 
+#include "expand_common.h"
 #include "internal.h"
 
 namespace caddtree {
@@ -70,7 +71,7 @@ accept_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict__ to
   }
   if (lane == 0) {
     accept_len[b] = alpha;
-    if (round_cost) round_cost[b] = (ns >= 0 && ns <= cap) ? ct.round(b)(ns) : NAN;
+    if (round_cost) round_cost[b] = (ns >= 0 && ns <= cap) ? xp::round_cost(ct, b)(ns) : NAN;
   }
 }
 

@@ -62,6 +62,16 @@ size_t elem_bytes(caddtree_dtype_t d) { return d == CADDTREE_BF16 ? 2 : 4; }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// The value a C caller stored in an enum-typed field or argument, read as the int it is: a C
+// caller may pass any int there, which a C++ enum object must not hold.
+template <typename E>
+int enum_value(const E& e) {
+  static_assert(sizeof(E) == sizeof(int), "the C enums of the interface are int-sized");
+  int v;
+  std::memcpy(&v, &e, sizeof v);
+  return v;
+}
+
 caddtree_status_t check_plan(const caddtree_plan* p) {
   if (p == nullptr) return fail(CADDTREE_E_INVALID, "plan is NULL");
   int dev = -1;
@@ -192,7 +202,7 @@ caddtree_status_t run_emit(const caddtree_plan* p, const int32_t* parent, const 
 extern "C" {
 
 const char* caddtree_status_string(caddtree_status_t s) {
-  switch (s) {
+  switch (enum_value(s)) {
     case CADDTREE_OK: return "ok";
     case CADDTREE_E_INVALID: return "invalid argument";
     case CADDTREE_E_UNSUPPORTED: return "unsupported configuration";
@@ -219,10 +229,11 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
   if (cfg->budget_cap < 0) return fail(CADDTREE_E_INVALID, "budget_cap = %d is negative", cfg->budget_cap);
   if (cfg->budget_cap > CADDTREE_MAX_CAP)
     return fail(CADDTREE_E_UNSUPPORTED, "budget_cap = %d exceeds %d", cfg->budget_cap, CADDTREE_MAX_CAP);
-  if (cfg->dtype != CADDTREE_F32 && cfg->dtype != CADDTREE_BF16)
-    return fail(CADDTREE_E_INVALID, "unknown dtype %d", (int)cfg->dtype);
-  if (cfg->mask != CADDTREE_MASK_NONE && cfg->mask != CADDTREE_MASK_U8 && cfg->mask != CADDTREE_MASK_BITS32)
-    return fail(CADDTREE_E_INVALID, "unknown mask kind %d", (int)cfg->mask);
+  const int dtype = enum_value(cfg->dtype), mask = enum_value(cfg->mask);
+  if (dtype != CADDTREE_F32 && dtype != CADDTREE_BF16)
+    return fail(CADDTREE_E_INVALID, "unknown dtype %d", dtype);
+  if (mask != CADDTREE_MASK_NONE && mask != CADDTREE_MASK_U8 && mask != CADDTREE_MASK_BITS32)
+    return fail(CADDTREE_E_INVALID, "unknown mask kind %d", mask);
   if (cfg->flags & ~(CADDTREE_ALLOW_NONCONVEX | CADDTREE_FIXED_BUDGET))
     return fail(CADDTREE_E_INVALID, "unknown flags 0x%x", cfg->flags);
   if (!(cfg->t_draft > 0.0) || !std::isfinite(cfg->t_draft))
@@ -277,8 +288,8 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
   p->V = cfg->V;
   p->K = cfg->K;
   p->cap = cap;
-  p->dtype = cfg->dtype;
-  p->mask = cfg->mask;
+  p->dtype = (caddtree_dtype_t)dtype;
+  p->mask = (caddtree_mask_t)mask;
   p->flags = cfg->flags;
   p->t_draft = cfg->t_draft;
   p->n_ctx = J;

@@ -14,6 +14,8 @@
 //     16-byte aligned) or 16-byte column groups (dense, each 16 bits spread to
 //     16 bytes), so every store instruction is coalesced.
 
+#include <hip/hip_runtime.h>
+
 #include "internal.h"
 
 namespace caddtree {

@@ -17,25 +17,17 @@
 #include <stdint.h>
 
 #include "caddtree.h"
+#include "kargs.h"
 
 namespace caddtree {
 
-// Mask and position ids written by an expansion kernel's epilogue (device pointers; both null when
-// the separate emission kernel writes them).
-struct EmitOut {
-  void* mask;          // [B, cap, cap] u8 or [B, cap, ceil(cap / 32)] u32, or null
-  int32_t* pos_ids;    // [B, cap], or null
-  int mask_kind;       // caddtree_mask_t
-  int pos_offset;
-  __host__ __device__ bool any() const { return mask != nullptr || pos_ids != nullptr; }
-  // round b's first mask row
-  __device__ void* round_mask(int b, int cap) const {
-    if (mask == nullptr || mask_kind == CADDTREE_MASK_NONE) return nullptr;
-    if (mask_kind == CADDTREE_MASK_BITS32)
-      return static_cast<uint32_t*>(mask) + (int64_t)b * cap * ((cap + 31) >> 5);
-    return static_cast<uint8_t*>(mask) + (int64_t)b * cap * cap;
-  }
-};
+// round b's first mask row of an epilogue's outputs (EmitOut is in kargs.h)
+__device__ __forceinline__ void* round_mask(const EmitOut& em, int b, int cap) {
+  if (em.mask == nullptr || em.mask_kind == CADDTREE_MASK_NONE) return nullptr;
+  if (em.mask_kind == CADDTREE_MASK_BITS32)
+    return static_cast<uint32_t*>(em.mask) + (int64_t)b * cap * ((cap + 31) >> 5);
+  return static_cast<uint8_t*>(em.mask) + (int64_t)b * cap * cap;
+}
 
 // LDS bytes of the bit tile for a tree of n nodes
 __host__ __device__ inline size_t emit_tile_bytes(int n) {

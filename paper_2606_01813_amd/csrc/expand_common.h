@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "kargs.h"
+
 namespace caddtree {
 namespace xp {
 
@@ -83,32 +85,23 @@ struct RoundCost {
   }
 };
 
-// The plan's cost tables as the kernels see them.
-struct CostTables {
-  const double* tv;        // [J, cap + 1]
-  const int64_t* grid;     // [J] strictly increasing context lengths (J >= 2), else unused
-  const int64_t* ctx_len;  // [B] context length of each round (J >= 2), else unused
-  int32_t J;
-  int32_t stride;          // cap + 1
-  double t_draft;
-
-  __device__ __forceinline__ RoundCost round(int64_t b) const {
-    RoundCost c{tv, tv, 0.0, t_draft};
-    if (J >= 2) {
-      const int64_t ell = ctx_len[b];
-      if (ell >= grid[J - 1]) {
-        c.lo = c.hi = tv + (int64_t)(J - 1) * stride;
-      } else if (ell > grid[0]) {
-        int j = 0;
-        while (grid[j + 1] <= ell) ++j;
-        c.lo = tv + (int64_t)j * stride;
-        c.hi = c.lo + stride;
-        c.alpha = (double)(ell - grid[j]) / (double)(grid[j + 1] - grid[j]);
-      }
+// The cost of round b (CostTables, the plan's tables as the kernels see them, is in kargs.h).
+__device__ __forceinline__ RoundCost round_cost(const CostTables& ct, int64_t b) {
+  RoundCost c{ct.tv, ct.tv, 0.0, ct.t_draft};
+  if (ct.J >= 2) {
+    const int64_t ell = ct.ctx_len[b];
+    if (ell >= ct.grid[ct.J - 1]) {
+      c.lo = c.hi = ct.tv + (int64_t)(ct.J - 1) * ct.stride;
+    } else if (ell > ct.grid[0]) {
+      int j = 0;
+      while (ct.grid[j + 1] <= ell) ++j;
+      c.lo = ct.tv + (int64_t)j * ct.stride;
+      c.hi = c.lo + ct.stride;
+      c.alpha = (double)(ell - ct.grid[j]) / (double)(ct.grid[j + 1] - ct.grid[j]);
     }
-    return c;
   }
-};
+  return c;
+}
 
 }  // namespace xp
 }  // namespace caddtree

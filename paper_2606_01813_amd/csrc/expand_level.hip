@@ -704,7 +704,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   const int LK = L * K;
   const bool lean = fixed || flat;          // no cost table
   const Lds s = carve(smem, (size_t)LK, (size_t)setcap, lean);
-  const RoundCost rc = ct.round(b);
+  const RoundCost rc = round_cost(ct, b);
 
   // setup: the round's global loads are issued together, then stored to LDS.  Indices are
   // clamped rather than guarded (a clamped lane loads and stores the same value as the last
@@ -941,7 +941,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   }
   __syncthreads();
   // the mask, in the set's (sigma, Lambda) region (free now; emit_tile_bytes(n) <= 16 setcap bytes)
-  emit_mask_wave(par, n, cap, em.mask_kind, em.round_mask(b, cap), reinterpret_cast<uint32_t*>(s.sl), lane);
+  emit_mask_wave(par, n, cap, em.mask_kind, round_mask(em, b, cap), reinterpret_cast<uint32_t*>(s.sl), lane);
 }
 
 }  // namespace

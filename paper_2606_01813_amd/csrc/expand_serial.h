@@ -229,7 +229,7 @@ __device__ __forceinline__ void expand_round(const Args& a, int b) {
   const int lane = threadIdx.x;
   const int LK = L * K;
   const Lds s = carve(smem, (size_t)LK, cap > 0 ? (size_t)cap : 1);
-  const RoundCost C = ct.round(b);
+  const RoundCost C = round_cost(ct, b);
 
   for (int i = lane; i < LK; i += kThreads) {
     s.tl[i] = topk_logit[(int64_t)b * LK + i];
@@ -485,7 +485,7 @@ __device__ __forceinline__ void expand_round(const Args& a, int b) {
   }
   __syncthreads();
   // the mask, in the key/heap region (free now; it holds emit_tile_bytes(n) <= 16 cap bytes)
-  emit_mask_wave(par, n, cap, a.em.mask_kind, a.em.round_mask(b, cap), reinterpret_cast<uint32_t*>(s.key), lane);
+  emit_mask_wave(par, n, cap, a.em.mask_kind, round_mask(a.em, b, cap), reinterpret_cast<uint32_t*>(s.key), lane);
 }
 
 }  // namespace serial

@@ -1,12 +1,13 @@
-// Internal launch interface between the host library (api.cpp) and the three kernels.
+// Internal launch interface between the host library (api.cpp) and the kernels.  Host-only sources
+// include it, so it declares no device code.
 #pragma once
 
-#include <hip/hip_runtime.h>
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
 #include <stdint.h>
 
 #include "caddtree.h"
-#include "emit_wave.h"
-#include "expand_common.h"
+#include "kargs.h"
 
 namespace caddtree {
 

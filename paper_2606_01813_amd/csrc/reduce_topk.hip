@@ -27,6 +27,7 @@
 #include <climits>
 #include <cmath>
 
+#include "expand_common.h"
 #include "internal.h"
 
 namespace caddtree {

@@ -9,6 +9,8 @@
 
 #include <mutex>
 
+#include <hip/hip_runtime.h>
+
 #include "internal.h"
 
 namespace caddtree {
