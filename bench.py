@@ -20,6 +20,13 @@ the drafter's marginals (``caddtree_accept``) and charged under the nominal
 cost model; prints one JSON line with time per token (sum C / sum (1 +
 alpha), in units of C_d), mean accepted length and mean budget per variant.
 
+Timing: the read-bandwidth probe runs first (its sweep brings the GPU to its working clocks), then
+W warm-up steps, then K steps back to back with HIP events on the launch stream before the first and
+after the last: ``value`` = B K / that time.  (An event between two steps leaves the GPU idle for
+several microseconds, so per-step events, recorded in a second pass, give only the distribution.)
+The roofline's kernel time is the average of K back-to-back launches of the vocabulary reduction
+between two events; a stage-by-stage pass gives the split between the three stages.
+
 Default workload c2: 1024 rounds x L=16 x V=151936 bf16 logits, K=8, cap 512,
 C_d = 1, C_v(n) = 1 + 0.002 n + 0.00002 n^2 (the HBM-saturating batch of the
 L=16 / V=151936 / bf16 rounds/sec metric).  Inputs are the seeded synthetic
@@ -286,6 +293,7 @@ def main():
     ap.add_argument("--workers", type=int, default=synth.gen.default_workers())
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-probe", action="store_true", help="skip the read-bandwidth probe (counter runs)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain elementwise copy of this many MiB (counter calibration)")
     ap.add_argument("--simulate", action="store_true",
@@ -345,7 +353,7 @@ def main():
 
     # the read probe first: its sweep streams the logits about a hundred times, so the GPU is at its
     # working clocks when the warm-up steps start
-    probe = read_probe(logits, cfg, stream)
+    probe = None if args.no_probe else read_probe(logits, cfg, stream)
     if probe:
         log(f"[bench] read probe {probe['us']:.1f} us = {probe['gbs']:.0f} GB/s "
             f"({probe['waves_per_row']} waves per row, {probe['unroll']} loads in flight)")
@@ -354,31 +362,41 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # timed region: K whole-path steps, each bracketed by HIP events on the launch stream
-    step_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(args.steps)]
+    # timed region: K whole-path steps back to back, HIP events on the launch stream before the first and
+    # after the last only (an event between steps leaves the GPU idle for several microseconds)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    gpu_step_us = ev0.elapsed_time(ev1) * 1e3 / args.steps
+    log(f"[bench] {args.steps} steps in {elapsed * 1e3:.2f} ms (wall); {gpu_step_us:.1f} us per step on the GPU")
+
+    # the same steps once more, each bracketed by its own events: the distribution of step times (each
+    # step then also carries the events' idle time)
+    step_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
     for a, b in step_ev:
         a.record(stream)
         step()
         b.record(stream)
     torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
     step_us = np.array([a.elapsed_time(b) for a, b in step_ev]) * 1e3
-    log(f"[bench] {args.steps} steps in {elapsed * 1e3:.2f} ms; median step {np.median(step_us):.1f} us")
 
-    # the vocabulary reduction alone, K launches back to back, each bracketed by HIP events on the launch
-    # stream: its average launch duration is the roofline's
+    # the vocabulary reduction alone, K launches back to back between two HIP events on the launch stream:
+    # their average duration is the roofline's
     topk = plan.new_outputs(B, topk=True)
-    k1_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-             for _ in range(args.steps)]
-    for a, b in k1_ev:
-        a.record(stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
         plan.reduce_topk(logits, topk.topk_ids, topk.topk_logit, topk.lse, topk.topk_lq, stream=stream)
-        b.record(stream)
+    e1.record(stream)
     torch.cuda.synchronize()
-    k1 = np.array([a.elapsed_time(b) for a, b in k1_ev]) * 1e3   # us
+    k1_avg = e0.elapsed_time(e1) * 1e3 / args.steps   # us
 
     # per-stage durations (the same work through the three stage entry points, interleaved)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
@@ -400,9 +418,9 @@ def main():
 
     rows = B * cfg.L
     k1_bytes = rows * cfg.V * cfg.elem_bytes + rows * (cfg.K * 12 + 8)
-    achieved = k1_bytes / (k1.mean() * 1e-6) / 1e9
+    achieved = k1_bytes / (k1_avg * 1e-6) / 1e9
     med_step = float(np.median(step_us))
-    value = B / (med_step * 1e-6)
+    value = B / (gpu_step_us * 1e-6)
     line = {
         "metric": METRIC,
         "value": value,
@@ -410,7 +428,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": med_step * 1e-3,
+        "ms_per_step": gpu_step_us * 1e-3,
         "wall_ms_per_step": elapsed * 1e3 / args.steps,
         "higher_is_better": True,
         "scaling": "weak",
@@ -426,19 +444,19 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(cfg.name),
                      "kernel": "reduce_topk_kernel", "bytes_per_launch": k1_bytes,
-                     "avg_launch_us": float(k1.mean()),
+                     "avg_launch_us": k1_avg,
                      "probe_gbs": probe["gbs"] if probe else None,
                      "pct_of_probe": achieved / probe["gbs"] if probe else None},
         "read_probe": probe,
         "cpu_baseline": cpu,
-        "reduce_topk_us": {"mean": float(k1.mean()), "median": float(np.median(k1)), "min": float(k1.min()),
-                           "max": float(k1.max())},
         "stages_us": {"reduce_topk": float(k1s.mean()), "expand": float(k2.mean()), "emit": float(k3.mean())},
         "stages_median_us": {"reduce_topk": float(np.median(k1s)), "expand": float(np.median(k2)),
                              "emit": float(np.median(k3))},
-        "step_us": {"median": med_step, "min": float(step_us.min()), "max": float(step_us.max()),
-                    "all": [round(float(x), 1) for x in step_us]},
-        "end_to_end_hbm_frac": cfg.batch_bytes / (med_step * 1e-6) / 1e9 / HBM_PEAK_GBS,
+        "step_us": {"gpu_mean": gpu_step_us,
+                    "with_per_step_events": {"median": med_step, "min": float(step_us.min()),
+                                             "max": float(step_us.max()), "rounds_per_s_at_median": B / (med_step * 1e-6),
+                                             "all": [round(float(x), 1) for x in step_us]}},
+        "end_to_end_hbm_frac": cfg.batch_bytes / (gpu_step_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
         "n_star": {"mean": float(ns.mean()), "std": float(ns.std()), "min": int(ns.min()), "max": int(ns.max()),
                    "histogram": nstar_histogram(ns)},
         "stage_path_matches_build": same,

@@ -298,7 +298,9 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
   __syncthreads();
   if (wave != 0) return;
 
-  if (S * K <= kWave) {
+  if (S == 1) {
+    // one wave per row: its list is the row's
+  } else if (S * K <= kWave) {
     // every wave's K best, one per lane: a lane's rank among them (ids are distinct) is its slot in
     // the merged list; only slots below K are needed, and those hold real entries
     const bool has = lane < S * K;

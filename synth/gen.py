@@ -87,32 +87,15 @@ def np_dtype(cfg: Config):
 
 # ---------------------------------------------------------------- batches
 
-_SHM = None  # worker-side handle
-
-
-def _worker_init(shm_name: str):
-    global _SHM
-    from multiprocessing import shared_memory
-    _SHM = shared_memory.SharedMemory(name=shm_name)
-
-
-def _worker_fill(args):
-    cfg, slot_rounds = args
-    out = np.ndarray((cfg.B, cfg.L, cfg.V), dtype=np_dtype(cfg), buffer=_SHM.buf)
-    for slot, b, a in slot_rounds:
-        out[slot] = draw_round(cfg, b, a)
-    del out
-    return len(slot_rounds)
-
-
 def draw_batch(cfg: Config, rounds: Optional[Sequence[int]] = None,
                attempts: Optional[Dict[int, int]] = None, workers: int = 1,
                out: Optional[np.ndarray] = None) -> np.ndarray:
     """Logits of a batch, shape [len(rounds), L, V].
 
     ``rounds`` defaults to ``range(cfg.B)``; ``attempts`` maps a round index to
-    its redraw attempt (default 0).  ``workers > 1`` fills the batch from a
-    pool of spawned processes through one shared-memory buffer.
+    its redraw attempt (default 0).  ``workers > 1`` fills the rounds from a
+    pool of threads (numpy's generators and ufuncs release the GIL), so no
+    child process is started.
     """
     rounds = list(range(cfg.B)) if rounds is None else list(rounds)
     attempts = attempts or {}
@@ -122,45 +105,24 @@ def draw_batch(cfg: Config, rounds: Optional[Sequence[int]] = None,
     if out is None:
         out = np.empty(shape, dtype=dt)
     assert out.shape == shape and out.dtype == dt
-    work = [(i, b, attempts.get(b, 0)) for i, b in enumerate(rounds)]
+
+    def fill(i: int) -> None:
+        b = rounds[i]
+        out[i] = draw_round(cfg, b, attempts.get(b, 0))
+
     workers = max(1, min(int(workers), n))
-    if workers == 1 or n < 4:
-        for i, b, a in work:
-            out[i] = draw_round(cfg, b, a)
+    if workers == 1:
+        for i in range(n):
+            fill(i)
         return out
-    import multiprocessing as mp
-    from multiprocessing import shared_memory
-    sub = cfg.replace(B=n)
-    shm = shared_memory.SharedMemory(create=True, size=max(1, out.nbytes))
-    try:
-        chunks = [work[k::workers] for k in range(workers)]
-        pool = mp.get_context("spawn").Pool(workers, initializer=_worker_init, initargs=(shm.name,))
-        try:
-            done = sum(pool.map(_worker_fill, [(sub, c) for c in chunks]))
-        finally:
-            pool.close()        # the workers exit on their own (no SIGTERM from terminate())
-            pool.join()
-        assert done == n
-        view = np.ndarray(shape, dtype=dt, buffer=shm.buf)
-        out[...] = view
-        del view
-    finally:
-        shm.close()
-        shm.unlink()
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(workers) as ex:
+        list(ex.map(fill, range(n)))
     return out
 
 
-def under_profiler() -> bool:
-    """True inside a rocprofv3 run: its launcher exports ROCPROF* variables, and a child process
-    would start the profiler (and, with counters, the GPU) again."""
-    return any(k.startswith("ROCPROF") for k in os.environ)
-
-
 def default_workers() -> int:
-    """Generator processes: every core this process may use, at most 16 (the host share of one GPU);
-    one (generate in this process) under the profiler."""
-    if under_profiler():
-        return 1
+    """Generator threads: every core this process may use, at most 16 (the host share of one GPU)."""
     try:
         n = len(os.sched_getaffinity(0))
     except AttributeError:  # pragma: no cover
