@@ -110,7 +110,14 @@ typedef struct {
 } caddtree_config_t;
 
 /* Validates cfg, copies the cost table to the current device and returns a plan.
- * The plan is bound to the device that is current at creation. */
+ * The plan holds what Algorithm 1 takes besides the marginals: K, the costs C_d
+ * and C_v(n; l) of Sec. 4.2 / 4.6 (eq. per-round's denominator), with the budget
+ * cap this library adds, and the launch layout.  Rejects a cost that breaks
+ * Assumption 1 (C_v non-decreasing and convex, Cor. 3) with CADDTREE_E_COST.
+ * The plan is bound to the device that is current at creation; *plan_out is
+ * NULL on any error.  Not thread-safe against caddtree_plan_destroy of the
+ * same plan; concurrent builds on one plan are safe (distinct outputs and
+ * workspaces). */
 caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_plan_t* plan_out);
 /* Frees the plan (NULL is a no-op).  The caller ensures no enqueued work still uses it. */
 void caddtree_plan_destroy(caddtree_plan_t plan);
@@ -156,7 +163,11 @@ typedef struct {
  * L_{J-1} table (no extrapolation, which could break convexity).  NULL is an
  * error for such plans and is allowed otherwise. */
 
-/* The whole hot path for B rounds: reduce + top-K, expansion, emission.
+/* The whole hot path for B rounds (Sec. 3.2-3.3 and Algorithm 1): per round the
+ * full-vocabulary log-normaliser and top-K of every position (eq. marginals),
+ * the best-first expansion with the greedy stop of Lemma 1 (eq. stopping; the
+ * tree T*_{n*} of eq. phistar at n* = the first maximiser of eq. per-round,
+ * Cor. 2), and the tree-attention mask and position ids (Sec. 3.3).
  * logits: DEVICE [B, L, row_stride] of the plan's dtype; B >= 0 (0 is a no-op).
  * workspace: DEVICE, >= caddtree_workspace_bytes(plan, B) bytes, 256-byte aligned
  * (may be NULL when every top-K output pointer is given).
