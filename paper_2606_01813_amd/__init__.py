@@ -322,8 +322,9 @@ class Plan:
         drawn from the uniforms ``u`` (float64 [B, L]); writes ``accept_len`` (int32 [B]) and optionally
         ``round_cost`` (float64 [B], this plan's C_d + C_v(n*))."""
         torch = _torch()
-        _check("token_ids", tree.token_ids, torch.int32, tree.token_ids.shape[1:] if tree.token_ids is not None
-               else (), 0, self.device)
+        if not isinstance(tree.token_ids, torch.Tensor) or tree.token_ids.dim() != 2:
+            raise ValueError("tree.token_ids must be a [B, tree_stride] tensor")
+        _check("token_ids", tree.token_ids, torch.int32, tree.token_ids.shape[1:], 0, self.device)
         B, stride = int(tree.token_ids.shape[0]), int(tree.token_ids.shape[1])
         _check("parent", tree.parent, torch.int32, (stride,), B, self.device)
         _check("n_star", tree.n_star, torch.int32, (), B, self.device)

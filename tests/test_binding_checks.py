@@ -178,6 +178,10 @@ def test_accept_checks(cpu_is_device):
     o2.parent = torch.zeros((B, CAP + 1), dtype=torch.int32)
     with pytest.raises(ValueError):
         p.accept(o, o2, u, al)
+    o3 = _outputs()
+    o3.token_ids = torch.zeros(B * CAP, dtype=torch.int32)
+    with pytest.raises(ValueError):
+        p.accept(o, o3, u, al)
 
 
 def test_valid_arguments_reach_the_library(cpu_is_device):
