@@ -32,6 +32,8 @@ struct caddtree_plan {
   int k1_unroll;        // 0 = automatic
   bool noalloc_ready;   // the scratch array of caddtree_build_noalloc has an address on this device
   bool fuse_emit;       // caddtree_build lets the expansion's epilogue write the mask and position ids
+  int first_rise;       // the batched expansion's first threshold inputs (ExpandArgs), -2 if per round
+  double tau_model;
 };
 
 namespace {
@@ -173,6 +175,8 @@ caddtree_status_t run_expand(const caddtree_plan* p, const int32_t* ids, const f
   a.level_set_cap = p->level_set_cap;
   a.fixed_budget = (p->flags & CADDTREE_FIXED_BUDGET) != 0;
   a.flat_cost = p->flat_cost;
+  a.first_rise = p->first_rise;
+  a.tau_model = p->tau_model;
   hipError_t e = caddtree::launch_expand(a, stream);
   if (e != hipSuccess) return hip_fail(e, "expand launch");
   return CADDTREE_OK;
@@ -308,6 +312,25 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
   p->flat_cost = flat_cost;
   p->use_level = cap >= 1 && (fixed || convex) && need <= caddtree::expand_level_max_need(lean);
   p->level_set_cap = caddtree::expand_level_set_cap(need, lean);
+  // With one cost table, where the batched expansion starts its threshold search depends on the
+  // plan only: the first position with a positive marginal cost (below the cap and the set
+  // capacity) and the cost-model threshold there, found once here instead of by every round.
+  // C(n) is formed as the kernels form it for one table, C_d + C_v(n).
+  p->first_rise = -2;
+  p->tau_model = 0.0;
+  if (J == 1 && !lean) {
+    const double* tv = cfg->t_verify_host;
+    const double td = cfg->t_draft;
+    const int mlim = std::min(cap, p->level_set_cap);
+    int m0 = -1;
+    for (int i = 0; i < mlim && m0 < 0; ++i)
+      if (td + tv[i + 1] > td + tv[i]) m0 = i;
+    p->first_rise = m0;
+    if (m0 >= 0) {
+      const int m = std::min(m0 + 32, cap);
+      p->tau_model = std::log(2.0 * ((td + tv[m0 + 1]) - (td + tv[m0])) / (td + tv[m])) - 0.5;
+    }
+  }
   if (const char* env = std::getenv("CADDTREE_EXPAND")) {
     if (std::strcmp(env, "serial") == 0) p->use_level = false;
   }

@@ -149,7 +149,8 @@ __device__ Lds carve(unsigned char* smem, size_t LK, size_t S, bool lean) {
 }
 
 // The cost table C(0 .. ncw - 1) in LDS is filled on demand, 64 entries at a time, so a round
-// reads from HBM (or L2) only the part of the table that its positions reach.
+// reads from memory only the part of the table that its positions reach (each distinct line
+// read adds to the round's latency).
 struct CostCache {
   const RoundCost rc;
   double* cw;
@@ -291,7 +292,7 @@ __device__ __forceinline__ int group_stop(int mA, double phA, double dA, int tA,
 }
 
 // Sets of 65 .. 64 P nodes held in registers (node e = j * 64 + lane): every node's position in
-// sigma order (ties by index) by one counting pass over the set, read from LDS as a broadcast;
+// sigma order (ties by index) by one counting pass over the set, each value read from its lane;
 // the path probabilities are scattered into that order, and the stop test runs at every
 // position in parallel, 64 positions at a time, with Phi carried across them.
 template <int P>
@@ -304,21 +305,29 @@ __device__ Stop stop_rank(const Lds& s, int ns, const StopTest& tst, int lane) {
     sg[j] = e < ns ? s.sl[e].x : -INFINITY;
     r[j] = 0;
   }
-  int o = 0;
-  for (; o + 4 <= ns; o += 4) {
-    double so[4];
+  // node o = jo * 64 + ol is read from its lane (jo is a compile-time index once unrolled); it
+  // precedes node e = j * 64 + lane if its sigma is larger, or equal with o < e, which holds for
+  // every o of an earlier block and for no o of a later one
 #pragma unroll
-    for (int u = 0; u < 4; ++u) so[u] = s.sl[o + u].x;
+  for (int jo = 0; jo < P; ++jo) {
+    const int lim = ns - jo * kW < kW ? ns - jo * kW : kW;   // wave-uniform
+    auto count = [&](double so, int ol) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+      for (int j = 0; j < P; ++j) {
+        if (jo < j) r[j] += (int)(so >= sg[j]);
+        else if (jo > j) r[j] += (int)(so > sg[j]);
+        else r[j] += (int)(so > sg[j]) | ((int)(so == sg[j]) & (int)(ol < lane));
+      }
+    };
+    int ol = 0;
+    for (; ol + 4 <= lim; ol += 4) {
+      double so[4];
 #pragma unroll
-      for (int j = 0; j < P; ++j)
-        r[j] += (int)(so[u] > sg[j]) | ((int)(so[u] == sg[j]) & (int)(o + u < j * kW + lane));
-  }
-  for (; o < ns; ++o) {
-    const double so = s.sl[o].x;
+      for (int u = 0; u < 4; ++u) so[u] = rl_d(sg[jo], ol + u);
 #pragma unroll
-    for (int j = 0; j < P; ++j) r[j] += (int)(so > sg[j]) | ((int)(so == sg[j]) & (int)(o < j * kW + lane));
+      for (int u = 0; u < 4; ++u) count(so[u], ol + u);
+    }
+    for (; ol < lim; ++ol) count(rl_d(sg[jo], ol), ol);
   }
 #pragma unroll
   for (int j = 0; j < P; ++j)
@@ -697,7 +706,8 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
                     int flat, int setcap, int32_t* __restrict__ token_ids,
                     int32_t* __restrict__ parent_out, int32_t* __restrict__ depth_out,
                     float* __restrict__ path_prob, int32_t* __restrict__ n_star_out,
-                    float* __restrict__ phi_out, float* __restrict__ theta_out, int in_place, EmitOut em) {
+                    float* __restrict__ phi_out, float* __restrict__ theta_out, int in_place, EmitOut em,
+                    int first_rise, double tau_model) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int b = blockIdx.x;
   const int lane = threadIdx.x;
@@ -752,14 +762,24 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
     tight = true;
     tau = top - drop_fixed(need);
   } else if (cap >= 1) {
-    // the first positive marginal cost c_{m0 + 1} (the stop lies past m0)
-    int m0 = -1;
-    const int mlim = cap < setcap ? cap : setcap;
-    for (int i0 = 0; i0 < mlim && m0 < 0; i0 += kW) {
-      const int i = i0 + lane;
-      cc.ensure(i0 + kW + 1, lane);
-      const unsigned long long m = __ballot(i < mlim && s.cw[i + 1] > s.cw[i]);
-      if (m) m0 = i0 + __builtin_ctzll(m);
+    // the first positive marginal cost c_{m0 + 1} (the stop lies past m0), and the cost-model
+    // threshold there: from the host for a plan with one cost table, else searched here
+    int m0 = first_rise;
+    double tau_cm = tau_model;
+    if (m0 < -1) {
+      m0 = -1;
+      const int mlim = cap < setcap ? cap : setcap;
+      for (int i0 = 0; i0 < mlim && m0 < 0; i0 += kW) {
+        const int i = i0 + lane;
+        cc.ensure(i0 + kW + 1, lane);
+        const unsigned long long m = __ballot(i < mlim && s.cw[i + 1] > s.cw[i]);
+        if (m) m0 = i0 + __builtin_ctzll(m);
+      }
+      if (m0 >= 0 && m0 < setcap / 2) {
+        const int m = m0 + 32 < cap ? m0 + 32 : cap;
+        cc.ensure(m + 1, lane);
+        tau_cm = log(2.0 * (s.cw[m0 + 1] - s.cw[m0]) / s.cw[m]) - 0.5;
+      }
     }
     if (m0 < 0 && cap <= setcap / 2) {
       need = cap;                           // flat up to the cap: every node is kept until the cap
@@ -775,9 +795,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       return;
     } else {
       need = m0 + 1;
-      const int m = m0 + 32 < cap ? m0 + 32 : cap;
-      cc.ensure(m + 1, lane);
-      tau = log(2.0 * (s.cw[m0 + 1] - s.cw[m0]) / s.cw[m]) - 0.5;
+      tau = tau_cm;
       if (need > 1) {
         tau -= kDropFlat;
         tight = true;
@@ -788,7 +806,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   const StopTest tst{cap, fixed, flat, c0, s.cw};
 
   int n = 0, ns = 0;
-  double phi = 0.0, theta = theta0;
+  double phi = 0.0;
   bool all_kept = false;                    // every node of T(tau) is kept (no flags written)
   bool done = cap == 0;
   bool failed = false;
@@ -818,18 +836,24 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
     int raises = 0;
     for (int d = 1; d < L && la < lb;) {
       const double Ad = rl_d(Areg, d + 1);
-      const double tlv = lane < K ? (double)s.tl[d * K + lane] : 0.0;   // lane r: rank r at depth d + 1
+      const int tli = d * K + (lane < K ? lane : K - 1);
       int nb = lb;
       bool over = false;
       for (int p0 = la; p0 < lb; p0 += kW) {
         const int p = p0 + lane;
         const bool live = p < lb;
         const double2 pv = s.sl[live ? p : la];
+        // lane r: rank r at depth d + 1, read after the parents (every lane reads a valid entry, so
+        // no branch holds the read back and the two reads overlap)
+        const double tlv = lane < K ? (double)s.tl[tli] : 0.0;
+        // the ranks that qualify form a prefix: count them rank by rank until no lane takes one
+        // (dead lanes compute too, on a valid node, and are masked out of the count)
         int c = 0, rmax = 0;
         for (; rmax < K; ++rmax) {
-          const bool q = live && (pv.y + rl_d(tlv, rmax)) - Ad >= tau;
-          if (__ballot(q) == 0) break;
-          c += q ? 1 : 0;
+          const double x = (pv.y + rl_d(tlv, rmax)) - Ad;
+          const int q = (int)(x >= tau) & (int)live;
+          if (__ballot(q != 0) == 0) break;
+          c += q;
         }
         const int incl = wave_incl_scan(c);
         const int tot = __builtin_amdgcn_readlane(incl, kW - 1);
@@ -837,17 +861,18 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
         if (live && c < K) cut = true;
         if (nb + tot > setcap) { over = true; break; }
         for (int r = 0; r < rmax; ++r) {
-          const double t = rl_d(tlv, r);
+          const double l = pv.y + rl_d(tlv, r);
+          const double2 v = make_double2(pmin(l - Ad, pv.x), l);
+          const uint32_t m = pack(p, r, d + 1);
           if (r < c) {
-            const int i = nb + off + r;
-            const double l = pv.y + t;
-            s.sl[i] = make_double2(pmin(l - Ad, pv.x), l);
-            s.meta[i] = pack(p, r, d + 1);
+            s.sl[nb + off + r] = v;
+            s.meta[nb + off + r] = m;
           }
         }
         nb += tot;
       }
       if (over) {
+        const double tlv = lane < K ? (double)s.tl[tli] : 0.0;
         const double t2 = ++raises > kMaxRaises ? NAN : raise_tau(s, la, lb, K, Ad, tlv, tau, top, keep_hi, need, lane);
         if (!(t2 > tau)) { failed = true; break; }
         tau = t2;
@@ -897,7 +922,6 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       }
       tau = target;
     }
-    if (done) theta = n == 0 ? theta0 : (1.0 + phi) / rc(n);
   }
   if (!done) {                              // left to the serial form
     if (in_place)
@@ -907,12 +931,17 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       n_star_out[b] = -1;
     return;
   }
+  // theta = (1 + Phi) / C(n): C(n) from the LDS table when the plan has one (every position up to
+  // min(ns, cap) + 1 is there), else from memory, a load whose wait falls at the end of the epilogue
+  const double cn = n == 0 ? c0 : (lean ? rc(n) : s.cw[n]);
   if (lane == 0) {
     n_star_out[b] = n;
     if (phi_out) phi_out[b] = (float)phi;
-    if (theta_out) theta_out[b] = (float)theta;
   }
-  if (n == 0) return;
+  if (n == 0) {
+    if (lane == 0 && theta_out) theta_out[b] = (float)theta0;
+    return;
+  }
 
   // ---- breadth-first positions: kept nodes before this one in generation order
   int base = 0;
@@ -942,6 +971,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   __syncthreads();
   // the mask, in the set's (sigma, Lambda) region (free now; emit_tile_bytes(n) <= 16 setcap bytes)
   emit_mask_wave(par, n, cap, em.mask_kind, round_mask(em, b, cap), reinterpret_cast<uint32_t*>(s.sl), lane);
+  if (lane == 0 && theta_out) theta_out[b] = (float)((1.0 + phi) / cn);
 }
 
 }  // namespace
@@ -972,7 +1002,7 @@ hipError_t launch_expand_level(const ExpandArgs& a, size_t in_place_lds, hipStre
   hipLaunchKernelGGL(expand_level_kernel, dim3((unsigned)a.B), dim3(kW), lds, stream, a.topk_ids, a.topk_logit,
                      a.lse, a.L, a.K, a.cap, a.cost, a.fixed_budget ? 1 : 0, (!a.fixed_budget && a.flat_cost) ? 1 : 0,
                      a.level_set_cap, a.token_ids, a.parent, a.depth, a.path_prob, a.n_star, a.phi, a.theta,
-                     in_place_lds > 0 ? 1 : 0, a.em);
+                     in_place_lds > 0 ? 1 : 0, a.em, a.first_rise, a.tau_model);
   return hipGetLastError();
 }
 

@@ -53,6 +53,9 @@ struct ExpandArgs {
   int32_t level_set_cap;   // its threshold-set capacity
   bool fixed_budget;       // no stop rule: keep the top min(cap, #nodes) nodes (DDTree)
   bool flat_cost;          // every table holds one value: C(n) = C(0) up to the cap
+  int32_t first_rise;      // one cost table: the first n < min(cap, level_set_cap) with C(n + 1) > C(n),
+                           // -1 if none; -2 when the kernel finds it per round (several tables)
+  double tau_model;        // with first_rise = m0 >= 0: log(2 (C(m0 + 1) - C(m0)) / C(min(m0 + 32, cap))) - 1/2
   EmitOut em;              // mask and position ids written by the expansion's epilogue (null: not here)
 };
 size_t expand_lds_bytes(int32_t L, int32_t K, int32_t cap);
