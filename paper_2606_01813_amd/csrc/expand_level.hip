@@ -35,9 +35,11 @@
 //       the bin that holds the stop is ranked node by node (or split again by
 //       a histogram of its own range when it holds more than 64 nodes);
 //     with a fixed budget m is kept iff m < cap;
-//  3. if every node of T(tau) is kept and the tree continues below tau, lower
-//     tau and start again; likewise when T(tau) holds fewer nodes than every
-//     tree keeps (a flat start of the cost, or a fixed budget).
+//  3. if every node of T(tau) is kept and the tree continues below tau, test
+//     the next pop, the frontier node of largest sigma: if it is not kept the
+//     stop falls right after T(tau); else lower tau and start again.  Lower
+//     tau likewise when T(tau) holds fewer nodes than every tree keeps (a flat
+//     start of the cost, or a fixed budget).
 //
 // The initial tau comes from the cost model: a node kept near position n has
 // delta > (1 + Phi) c_{n+1} / C(n) (Lemma 1); with c_{m0+1} the first positive
@@ -695,6 +697,47 @@ __device__ double raise_tau(const Lds& s, int& la, int& lb, int K, double Ad, do
   return t2;
 }
 
+// The largest sigma among the nodes outside the set s[0, ns) = T(tau), where every node of the set is
+// kept and the tree continues: the next pop, whose delta decides whether the stop falls right after
+// the set.  Every node outside T(tau) descends from, or is a later sibling of, a frontier node (the
+// first child of a node with no child in the set, or the next sibling of a node that is its
+// parent's last child in the set; siblings are contiguous in generation order), and sigma does not
+// rise along either step, so the largest sigma outside is the largest over the frontier.  Each
+// frontier node's sigma is formed as the build forms a child's.  Uses s.pos as scratch.  The
+// caller reads the result through readlane: the compiler cannot see that the butterfly leaves it
+// wave-uniform, and a value it takes for divergent would make the attempt loop's control
+// divergent after it.
+__device__ double frontier_max(const Lds& s, int ns, int L, int K, double Areg, int lane) {
+  for (int i = lane; i < ns; i += kW) s.pos[i] = 0;
+  for (int i = lane; i < ns; i += kW) {
+    const int p = m_parent(s.meta[i]);
+    if (p >= 0) s.pos[p] = 1;               // p has a child in the set
+  }
+  double best = -INFINITY;
+  for (int i0 = 0; i0 < ns; i0 += kW) {
+    const int i = i0 + lane;
+    const bool live = i < ns;
+    const int ii = live ? i : 0;
+    const uint32_t m = s.meta[ii];
+    const int p = m_parent(m), r = m_rank(m), d = m_depth(m);
+    const double2 v = s.sl[ii];
+    const double Ad = __shfl(Areg, d);            // A_d
+    const double Ad1 = __shfl(Areg, d < L ? d + 1 : d);
+    if (live && d < L && s.pos[ii] == 0) {        // first child: rank 0 at depth d + 1
+      const double l = v.y + (double)s.tl[d * K];
+      best = fmax(best, pmin(l - Ad1, v.x));
+    }
+    const bool last = i + 1 >= ns || m_parent(s.meta[i + 1 < ns ? i + 1 : ii]) != p;
+    if (live && last && r + 1 < K) {              // next sibling: rank r + 1 at depth d
+      const double2 pv = p < 0 ? make_double2(0.0, 0.0) : s.sl[p];   // the root: sigma 0, Lambda 0
+      const double l = pv.y + (double)s.tl[(d - 1) * K + r + 1];
+      best = fmax(best, pmin(l - Ad, pv.x));
+    }
+  }
+  for (int k = 1; k < kW; k <<= 1) best = fmax(best, __shfl_xor(best, k));
+  return best;   // the same in every lane (the caller reads it as a wave-uniform value)
+}
+
 // A round the batched form cannot settle, run by the serial form in the same workgroup (the
 // launch reserved LDS for the serial layout).  Out of line: it is rare, and inlined it would
 // crowd the batched kernel's registers.
@@ -904,7 +947,10 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       phi = st.phi;
       all_kept = false;
       done = true;
-    } else if (!cut || ns >= cap) {         // the whole tree (or the cap) is here and all of it is kept
+    } else if (!cut || ns >= cap ||
+               !kept_at(ns, st.phi, exp(rl_d(frontier_max(s, ns, L, K, Areg, lane), 0)), tst)) {
+      // the whole tree (or the cap) is here and all of it is kept, or the next pop (the frontier
+      // node of largest sigma) is not kept: the stop falls right after the set
       n = ns;
       phi = st.phi;
       all_kept = true;
