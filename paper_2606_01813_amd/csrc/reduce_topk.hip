@@ -61,10 +61,20 @@ __device__ __forceinline__ int readlane_i(int v, int l) { return __builtin_amdgc
 __device__ __forceinline__ int shr1(int v) { return __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, true); }
 __device__ __forceinline__ float shr1f(float v) { return __int_as_float(shr1(__float_as_int(v))); }
 
+// the maximum over the wave, wave-uniform: a DPP max-scan (row shifts, then row broadcasts; a lane
+// with no source keeps its own value), whose last lane holds the total
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_keep(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL, ROW_MASK, 0xF, false));
+}
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+  v = fmaxf(v, dpp_keep<0x111, 0xF>(v));
+  v = fmaxf(v, dpp_keep<0x112, 0xF>(v));
+  v = fmaxf(v, dpp_keep<0x114, 0xF>(v));
+  v = fmaxf(v, dpp_keep<0x118, 0xF>(v));
+  v = fmaxf(v, dpp_keep<0x142, 0xA>(v));
+  v = fmaxf(v, dpp_keep<0x143, 0xC>(v));
+  return readlane_f(v, kWave - 1);
 }
 
 // (v, id) goes before (w, wid) in the order value desc, id asc
@@ -155,19 +165,19 @@ __device__ __forceinline__ void chunk_full(WaveState& s, const float (&x)[VEC], 
   const bool cand = cmax >= s.thr;
   const bool any = __ballot(cand) != 0;
   if (__builtin_expect(any, 0)) rare<VEC>(s, x, (1u << VEC) - 1u, cmax, base, K);
-  float t[VEC];
+  float t[VEC], p[VEC];
 #pragma unroll
-  for (int j = 0; j < VEC; ++j) t[j] = term(x[j], s.r);
+  for (int j = 0; j < VEC; ++j) p[j] = t[j] = term(x[j], s.r);
 #pragma unroll
   for (int w = 1; w < VEC; w <<= 1)
 #pragma unroll
-    for (int j = 0; j + w < VEC; j += 2 * w) t[j] += t[j + w];
-  s.acc += (double)t[0];
+    for (int j = 0; j + w < VEC; j += 2 * w) p[j] += p[j + w];
+  s.acc += (double)p[0];
   if (__builtin_expect(any, 0) && cand) {
     double e = 0.0;
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) e += (double)term(x[j], s.r);
-    s.acc += e - (double)t[0];
+    for (int j = 0; j < VEC; ++j) e += (double)t[j];
+    s.acc += e - (double)p[0];
   }
 }
 
