@@ -20,8 +20,8 @@ LIB = os.path.join(PKG, "libcaddtree.so")
 # the benchmark's read-bandwidth probe: a library of its own, outside the CaDDTree interface
 PROBE_LIB = os.path.join(PKG, "libcaddtree_probe.so")
 PROBE_SOURCES = ["probe.hip"]
-SOURCES = ["api.cpp", "reduce_topk.hip", "expand.hip", "expand_level.hip", "emit.hip", "accept.hip", "scratch.hip",
-           "costfit.cpp"]
+SOURCES = ["api.cpp", "reduce_topk.hip", "expand.hip", "expand_level.hip", "expand_wide.hip", "emit.hip", "accept.hip",
+           "scratch.hip", "costfit.cpp"]
 ARCH = os.environ.get("CADDTREE_ARCH", "gfx950")
 
 

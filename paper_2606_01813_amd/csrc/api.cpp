@@ -25,6 +25,7 @@ struct caddtree_plan {
   double* d_t_verify;   // device copy, n_ctx x (cap + 1) values
   int64_t* d_ctx_grid;  // device copy of the grid (n_ctx >= 2), else NULL
   bool use_level;       // the batched expansion applies (see plan_create)
+  bool use_wide;        // ... in its several-wavefront form
   bool flat_cost;       // every cost table holds one value up to the cap
   int level_set_cap;    // its threshold-set capacity
   int device;
@@ -172,6 +173,7 @@ caddtree_status_t run_expand(const caddtree_plan* p, const int32_t* ids, const f
   a.phi = phi;
   a.theta = theta;
   a.use_level = p->use_level;
+  a.use_wide = p->use_wide;
   a.level_set_cap = p->level_set_cap;
   a.fixed_budget = (p->flags & CADDTREE_FIXED_BUDGET) != 0;
   a.flat_cost = p->flat_cost;
@@ -331,8 +333,13 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
       p->tau_model = std::log(2.0 * ((td + tv[m0 + 1]) - (td + tv[m0])) / (td + tv[m])) - 0.5;
     }
   }
+  // Large trees of a known size (fixed budgets and costs flat up to the cap, 512 nodes or more) run
+  // on eight wavefronts per round; CADDTREE_EXPAND=level keeps them on one, =serial sends every
+  // round to the serial kernel.
+  p->use_wide = p->use_level && caddtree::expand_wide_applies(cap, lean);
   if (const char* env = std::getenv("CADDTREE_EXPAND")) {
     if (std::strcmp(env, "serial") == 0) p->use_level = false;
+    if (std::strcmp(env, "level") == 0) p->use_wide = false;
   }
   // The expansion kernels can write each round's mask and position ids from the tree still in LDS,
   // one wavefront per round, which saves a launch.  That pays for the trees a rising cost keeps small;
@@ -368,6 +375,7 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
   (void)hipGetLastError();
   if (e == hipSuccess) e = caddtree::expand_prepare(p->L, p->K, p->cap);
   if (e == hipSuccess) e = caddtree::expand_level_prepare();
+  if (e == hipSuccess) e = caddtree::expand_wide_prepare();
   if (e != hipSuccess) {
     (void)hipFree(p->d_t_verify);
     if (p->d_ctx_grid) (void)hipFree(p->d_ctx_grid);

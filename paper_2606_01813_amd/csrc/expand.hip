@@ -34,7 +34,12 @@ hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream) {
   if (a.B == 0) return hipSuccess;
   int only_flagged = 0;
   const size_t lds = expand_lds_bytes(a.L, a.K, a.cap);
-  if (a.use_level) {
+  if (a.use_level && a.use_wide) {
+    // the several-wavefront form flags the rounds it cannot settle; the serial kernel follows
+    const hipError_t e = launch_expand_wide(a, stream);
+    if (e != hipSuccess) return e;
+    only_flagged = 1;
+  } else if (a.use_level) {
     // The batched kernel runs a round it cannot settle in place when the serial layout needs at
     // most kInPlaceLds bytes; otherwise it flags the round and the serial kernel follows.
     const bool in_place = lds <= kInPlaceLds;

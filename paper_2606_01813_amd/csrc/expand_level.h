@@ -417,6 +417,55 @@ __device__ __forceinline__ double dkey_inv(unsigned long long k) {
 }
 constexpr double kFix = 0x1p50;   // fixed-point scale of delta in the bin sums (at most 4096 * 2^50 < 2^63)
 
+// The stop inside the bin that holds it, of t <= 64 nodes: mem[0 .. t) are the bin's nodes in
+// generation order, mk the position of its first node in the pop order and pk Phi before it.
+// Ranks them by sigma (ties by index), tests every position, and marks each of them kept (1) or
+// not (0) in s.pos; a tie group cut by the stop is ordered by the full pop order.  Uses s.hsum as
+// scratch.
+__device__ __forceinline__ Stop stop_in_bin(const Lds& s, const int* mem, int t, int mk, double pk, int ns,
+                                            const StopTest& tst, int lane) {
+  const bool live = lane < t;
+  const int me = mem[live ? lane : 0];
+  const double sg = live ? s.sl[me].x : -INFINITY;
+  int r = 0;
+  for (int o = 0; o < t; ++o) {
+    const double so = rl_d(sg, o);
+    r += (int)(so > sg) | ((int)(so == sg) & (int)(o < lane));
+  }
+  double* ds = reinterpret_cast<double*>(s.hsum);   // delta of the bin's nodes in sigma order
+  if (live) ds[r] = s.dl[me];
+  const double d = live ? ds[lane] : 0.0;
+  const double incl = wave_incl_scan(d);
+  const double pe = pk + wave_shr1(incl);           // Phi before position mk + lane
+  const bool keep = live && kept_at(mk + lane, pe, d, tst);
+  const unsigned long long fm = __ballot(live && !keep);
+  const int ks = fm ? __builtin_ctzll(fm) : t;
+  const int n = mk + ks;
+  const double phi = fm ? rl_d(pe, ks) : pk + rl_d(incl, kW - 1);
+  if (n == ns) return Stop{ns, phi, true};
+  int kept = 1;
+  if (ks < t) {
+    const double v = rl_d(sg, __builtin_ctzll(__ballot(live && r == ks)));   // sigma at the stop
+    const int g0 = __popcll(__ballot(live && sg > v));
+    kept = r < ks;
+    if (g0 < ks) {                      // the stop cuts a tie group: its full pop order decides
+      const double lam = live ? s.sl[me].y : 0.0;
+      const uint32_t mm = live ? s.meta[me] : 0u;
+      int rt = 0;
+      for (int o = 0; o < t; ++o) {
+        const double so = rl_d(sg, o);
+        if (so == v)
+          rt += (live && sg == v &&
+                 pops_before(v, rl_d(lam, o), rl_u(mm, o), __builtin_amdgcn_readlane(me, o), v, lam, mm, me))
+                    ? 1 : 0;
+      }
+      kept = sg > v || (sg == v && g0 + rt < ks);
+    }
+  }
+  if (live) s.pos[me] = kept ? 1 : 0;
+  return Stop{n, phi, false};
+}
+
 // Sets above 128 nodes, in LDS.  A 64-bin histogram over the range of sigma gives, per bin,
 // the node count, the largest and smallest sigma and the sum of delta in fixed point
 // (integer atomics, so the sums do not depend on the order of the additions; their error,
@@ -511,46 +560,7 @@ __device__ Stop stop_hist(const Lds& s, int ns, const StopTest& tst, double lo, 
         nb += __popcll(gm);
       }
     }
-    const bool live = lane < t;
-    const int me = mem[live ? lane : 0];
-    const double sg = live ? s.sl[me].x : -INFINITY;
-    int r = 0;
-    for (int o = 0; o < t; ++o) {
-      const double so = rl_d(sg, o);
-      r += (int)(so > sg) | ((int)(so == sg) & (int)(o < lane));
-    }
-    double* ds = reinterpret_cast<double*>(s.hsum);   // delta of the bin's nodes in sigma order
-    if (live) ds[r] = s.dl[me];
-    const double d = live ? ds[lane] : 0.0;
-    const double incl = wave_incl_scan(d);
-    const double pe = pk + wave_shr1(incl);           // Phi before position mk + lane
-    const bool keep = live && kept_at(mk + lane, pe, d, tst);
-    const unsigned long long fm = __ballot(live && !keep);
-    const int ks = fm ? __builtin_ctzll(fm) : t;
-    const int n = mk + ks;
-    const double phi = fm ? rl_d(pe, ks) : pk + rl_d(incl, kW - 1);
-    if (n == ns) return Stop{ns, phi, true};
-    int kept = 1;
-    if (ks < t) {
-      const double v = rl_d(sg, __builtin_ctzll(__ballot(live && r == ks)));   // sigma at the stop
-      const int g0 = __popcll(__ballot(live && sg > v));
-      kept = r < ks;
-      if (g0 < ks) {                      // the stop cuts a tie group: its full pop order decides
-        const double lam = live ? s.sl[me].y : 0.0;
-        const uint32_t mm = live ? s.meta[me] : 0u;
-        int rt = 0;
-        for (int o = 0; o < t; ++o) {
-          const double so = rl_d(sg, o);
-          if (so == v)
-            rt += (live && sg == v &&
-                   pops_before(v, rl_d(lam, o), rl_u(mm, o), __builtin_amdgcn_readlane(me, o), v, lam, mm, me))
-                      ? 1 : 0;
-        }
-        kept = sg > v || (sg == v && g0 + rt < ks);
-      }
-    }
-    if (live) s.pos[me] = kept ? 1 : 0;
-    return Stop{n, phi, false};
+    return stop_in_bin(s, mem, t, mk, pk, ns, tst, lane);
   }
   return stop_lds(s, ns, tst, lane, seed);
 }

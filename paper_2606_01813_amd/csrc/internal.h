@@ -50,6 +50,7 @@ struct ExpandArgs {
   float* phi;              // optional
   float* theta;            // optional
   bool use_level;          // try the batched kernel first
+  bool use_wide;           // ... in its several-wavefront form (large trees of a known size)
   int32_t level_set_cap;   // its threshold-set capacity
   bool fixed_budget;       // no stop rule: keep the top min(cap, #nodes) nodes (DDTree)
   bool flat_cost;          // every table holds one value: C(n) = C(0) up to the cap
@@ -72,6 +73,13 @@ size_t expand_level_lds_bytes(int32_t L, int32_t K, int32_t set_cap, bool lean);
 int expand_level_set_cap(int32_t need, bool lean);   // threshold-set capacity for trees of at least `need` nodes
 int expand_level_max_need(bool lean);                // the largest `need` the batched kernel takes
 hipError_t expand_level_prepare();        // raises the batched kernel's dynamic-LDS limit
+// The several-wavefront batched kernel (expand_wide.hip): trees that keep a known number of nodes
+// (a fixed budget, or a cost flat up to the cap) of at least 512.  Rounds it cannot settle are
+// flagged n_star = -1 for the serial kernel.
+bool expand_wide_applies(int32_t cap, bool lean);
+size_t expand_wide_lds_bytes(int32_t L, int32_t K, int32_t set_cap);
+hipError_t expand_wide_prepare();
+hipError_t launch_expand_wide(const ExpandArgs& a, hipStream_t stream);
 
 // Stage 3: mask and position ids.
 struct EmitArgs {

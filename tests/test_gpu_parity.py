@@ -717,6 +717,54 @@ def test_fixed_budget_paths_agree(monkeypatch):
     _paths_agree(outs)
 
 
+@pytest.mark.parametrize("name,kw", [
+    ("c1f1024", dict(V=3000, B=12)),                          # fixed budget, 2048-node set
+    ("c1", dict(V=2000, B=8, cap=512, fixed=True)),           # the smallest budget on eight wavefronts
+    ("c1", dict(V=2000, B=6, cap=4096, fixed=True)),          # the largest budget, 5120-node set
+    ("s1", dict(V=2000, B=6)),                                # cost flat to the cap 4096
+    ("s1", dict(V=2000, B=8, L=12, cap=700)),                 # flat cost, shorter trees
+])
+def test_wide_and_one_wave_kernels_agree(name, kw, monkeypatch):
+    """Large trees of a known size run on eight wavefronts per round; the one-wavefront kernel
+    (CADDTREE_EXPAND=level) and the serial kernel give the same trees."""
+    cfg = synth.get_config(name).replace(**kw)
+    xs = synth.draw_batch(cfg)
+    lg = torch_logits(cfg, xs)
+    outs = {}
+    for mode in ("auto", "level", "serial"):
+        if mode == "auto":
+            monkeypatch.delenv("CADDTREE_EXPAND", raising=False)
+        else:
+            monkeypatch.setenv("CADDTREE_EXPAND", mode)
+        outs[mode] = host(run_build(make_plan(cfg), lg))
+    say(f"[wide] {cfg.name} cap {cfg.cap} n* {outs['auto']['n_star'].tolist()}")
+    _paths_agree({"auto": outs["auto"], "serial": outs["level"]})
+    _paths_agree({"auto": outs["auto"], "serial": outs["serial"]})
+
+
+def test_wide_kernel_on_ties(monkeypatch):
+    """Logits on a 0.5 grid (many nodes tie on sigma and on Lambda): the eight-wavefront kernel's
+    raises, histogram splits and cut tie groups give the one-wavefront kernel's trees."""
+    import torch
+    cfg = synth.get_config("c4").replace(V=1500, B=48, L=8, K=16, cost="c4", cap=600, fixed=True)
+    rng = np.random.default_rng(12)
+    x = np.round(rng.standard_normal((cfg.B, cfg.L, cfg.V)) * 2.0) / 2.0
+    peak = rng.integers(0, cfg.V, size=(cfg.B, cfg.L))
+    x[np.arange(cfg.B)[:, None], np.arange(cfg.L)[None, :], peak] += rng.choice([0.0, 3.0, 6.0], size=(cfg.B, cfg.L))
+    lg = torch_logits(cfg, x.astype(np.float32))
+    for c in (cfg, cfg.replace(cost="const", fixed=False)):
+        outs = {}
+        for mode in ("auto", "level"):
+            if mode == "auto":
+                monkeypatch.delenv("CADDTREE_EXPAND", raising=False)
+            else:
+                monkeypatch.setenv("CADDTREE_EXPAND", mode)
+            outs[mode] = host(run_build(make_plan(c), lg))
+        n = outs["auto"]["n_star"]
+        say(f"[wide ties] {c.cost} fixed={c.fixed} n* mean {n.mean():.1f} min {n.min()} max {n.max()}")
+        _paths_agree({"auto": outs["auto"], "serial": outs["level"]})
+
+
 def test_fixed_budget_is_top_n_of_the_greedy_tree():
     """The fixed-budget tree at n* of the greedy stop is the greedy tree itself (Prop. 1: T*_n nest)."""
     cfg = synth.get_config("c1").replace(V=6000, B=8)

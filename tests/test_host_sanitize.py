@@ -136,8 +136,8 @@ def sanitized(tmp_path_factory):
     if gxx is None:
         pytest.skip("g++ is not available")
     objs = os.path.join(PKG, "_build")
-    device_objs = [os.path.join(objs, n) for n in ("reduce_topk.o", "expand.o", "expand_level.o", "emit.o",
-                                                    "accept.o", "scratch.o")]
+    from paper_2606_01813_amd import _build
+    device_objs = [os.path.join(objs, os.path.splitext(n)[0] + ".o") for n in _build.SOURCES if n.endswith(".hip")]
     missing = [o for o in device_objs if not os.path.exists(o)]
     if missing:
         pytest.fail(f"build the library first (python -m paper_2606_01813_amd._build): {missing}")
