@@ -26,6 +26,7 @@ struct caddtree_plan {
   int64_t* d_ctx_grid;  // device copy of the grid (n_ctx >= 2), else NULL
   bool use_level;       // the batched expansion applies (see plan_create)
   bool use_wide;        // ... in its several-wavefront form
+  int num_cu;           // compute units of the plan's device
   bool flat_cost;       // every cost table holds one value up to the cap
   int level_set_cap;    // its threshold-set capacity
   int device;
@@ -174,6 +175,7 @@ caddtree_status_t run_expand(const caddtree_plan* p, const int32_t* ids, const f
   a.theta = theta;
   a.use_level = p->use_level;
   a.use_wide = p->use_wide;
+  a.num_cu = p->num_cu;
   a.level_set_cap = p->level_set_cap;
   a.fixed_budget = (p->flags & CADDTREE_FIXED_BUDGET) != 0;
   a.flat_cost = p->flat_cost;
@@ -361,6 +363,8 @@ caddtree_status_t caddtree_plan_create(const caddtree_config_t* cfg, caddtree_pl
   }
   hipError_t e = hipGetDevice(&p->device);
   if (e != hipSuccess) { delete p; return hip_fail(e, "hipGetDevice"); }
+  e = hipDeviceGetAttribute(&p->num_cu, hipDeviceAttributeMultiprocessorCount, p->device);
+  if (e != hipSuccess) { delete p; return hip_fail(e, "hipDeviceGetAttribute(multiprocessor count)"); }
   const size_t tv_bytes = sizeof(double) * (size_t)J * (size_t)(cap + 1);
   e = hipMalloc(&p->d_t_verify, tv_bytes);
   if (e != hipSuccess) { delete p; return hip_fail(e, "hipMalloc(cost table)"); }

@@ -3,14 +3,14 @@
 // plans whose trees keep a known number of nodes before any stop test -- fixed
 // budgets (the DDTree construction, Sec. 3.4) and costs flat up to the cap --
 // when that number is 512 or more.  A one-wavefront round of 4096 nodes keeps
-// one SIMD of its CU busy and leaves the rest idle; here eight wavefronts
+// one SIMD of its CU busy and leaves the rest idle; here 8 or 16 wavefronts
 // share each pass over a level or over the set.
 //
 // The steps are those of the one-wavefront kernel (expand_level.hip): build
 // T(tau) level by level, raise tau in place when a level overflows the set,
 // lower it when the set is too small, find the stop by a histogram of sigma,
 // then lay the kept nodes out in breadth-first order.  Each pass is split into
-// 64-node chunks, chunk k going to wavefront k mod 8; the steps that need the
+// 64-node chunks, chunk k going to wavefront k mod NW; the steps that need the
 // whole set or level (slot offsets of a level's children, histogram totals,
 // new indices after a compaction, breadth-first positions) meet at workgroup
 // barriers, with per-chunk counts in LDS.
@@ -29,8 +29,6 @@ namespace caddtree {
 namespace {
 
 constexpr int kWideMinNodes = 512;         // trees of at least this many nodes
-constexpr int kWideWaves = 8;
-constexpr int kWideThreads = kWideWaves * kW;
 constexpr int kMaxChunks = 2 * kW;          // chunk counts held by two lanes' worth per wavefront
 constexpr int kWideBins = 1024;             // histogram bins of the in-place raise
 static_assert((kMaxLeanSet + kW - 1) / kW <= kMaxChunks, "a set's chunk counts fit the prefix");
@@ -77,6 +75,7 @@ __device__ __forceinline__ ChunkPrefix chunk_prefix(const WideShared& x, int nch
 // keep_hi nodes over depths 1 .. d + 1 and, as far as the histogram resolves, at least need;
 // then the order-preserving compaction of s[0, lb) to the nodes that reach it, with parents
 // renumbered.  Called by every thread of the workgroup; returns tau' (NaN: none found).
+template <int NW>
 __device__ double wide_raise(const Lds& s, WideShared& x, int& la, int& lb, int K, int d, double Ad, double tau,
                              double top, int keep_hi, int need, int lane, int w, int tid) {
   int* hb = reinterpret_cast<int*>(s.dl);   // free while the set is built: 1024 bins
@@ -93,14 +92,14 @@ __device__ double wide_raise(const Lds& s, WideShared& x, int& la, int& lb, int 
       return b < kWideBins - 1 ? b : kWideBins - 1;
     };
     __syncthreads();                         // the previous pass's readers are done with the bins
-    for (int i = tid; i < kWideBins; i += kWideThreads) hb[i] = 0;
+    for (int i = tid; i < kWideBins; i += (NW * kW)) hb[i] = 0;
     __syncthreads();
-    for (int i = tid; i < lb; i += kWideThreads) {
+    for (int i = tid; i < lb; i += (NW * kW)) {
       const double v = s.sl[i].x;
       if (v >= lo_e && (first || v < hi_e)) atomicAdd(&hb[bin(v)], 1);
     }
     const int nchk = (lb - la + kW - 1) / kW;
-    for (int k = w; k < nchk; k += kWideWaves) {   // the next level's candidates
+    for (int k = w; k < nchk; k += NW) {   // the next level's candidates
       const int p = la + k * kW + lane;
       const bool live = p < lb;
       const double2 pv = s.sl[live ? p : la];
@@ -154,7 +153,7 @@ __device__ double wide_raise(const Lds& s, WideShared& x, int& la, int& lb, int 
   const int n0 = lb;
   const int nchk = (n0 + kW - 1) / kW;
   __syncthreads();                           // every reader of the bins and chunk counts is done
-  for (int k = w; k < nchk; k += kWideWaves) {
+  for (int k = w; k < nchk; k += NW) {
     const int i = k * kW + lane;
     const bool keep = i < n0 && s.sl[i < n0 ? i : 0].x >= t2;
     const unsigned long long km = __ballot(keep);
@@ -165,7 +164,7 @@ __device__ double wide_raise(const Lds& s, WideShared& x, int& la, int& lb, int 
   }
   __syncthreads();
   const ChunkPrefix pre = chunk_prefix(x, nchk, lane);
-  for (int k = w; k < nchk; k += kWideWaves) {
+  for (int k = w; k < nchk; k += NW) {
     const int i = k * kW + lane;
     const bool live = i < n0;
     const bool keep = live && s.sl[live ? i : 0].x >= t2;
@@ -176,7 +175,7 @@ __device__ double wide_raise(const Lds& s, WideShared& x, int& la, int& lb, int 
   __syncthreads();                           // every new index is written
   // a kept node moves from i to j <= i: each round reads one chunk per wavefront, then writes it;
   // a later round reads only indices above every index an earlier round wrote
-  for (int q0 = 0; q0 < nchk; q0 += kWideWaves) {
+  for (int q0 = 0; q0 < nchk; q0 += NW) {
     const int k = q0 + w;
     const int i = k * kW + lane;
     int j = -1, np = -1;
@@ -207,6 +206,7 @@ __device__ double wide_raise(const Lds& s, WideShared& x, int& la, int& lb, int 
 // the histograms and the classification passes split over the wavefronts and the stop inside
 // its bin found by wavefront 0.  Returns false (fallback) when no bin of at most 64 nodes holds
 // the stop within kLevels splits; then the caller runs the bisection on wavefront 0.
+template <int NW>
 __device__ bool wide_hist(const Lds& s, WideShared& x, int ns, const StopTest& tst, double lo, double hi, int lane,
                           int w, int tid, Stop& out) {
   int base_m = 0;
@@ -227,7 +227,7 @@ __device__ bool wide_hist(const Lds& s, WideShared& x, int ns, const StopTest& t
       s.hsum[lane] = 0ull;
     }
     __syncthreads();
-    for (int e = tid; e < ns; e += kWideThreads) {
+    for (int e = tid; e < ns; e += (NW * kW)) {
       if (open(e)) {
         const double v = s.sl[e].x;
         double dd;
@@ -262,7 +262,7 @@ __device__ bool wide_hist(const Lds& s, WideShared& x, int ns, const StopTest& t
     const unsigned long long full = __ballot(cnt > 0);
     const unsigned long long above = fails ? full & ~((2ull << (63 - __builtin_clzll(fails))) - 1ull) : full;
     if (above == 0) {                        // the open range's first node is not kept (level 0 only)
-      for (int e = tid; e < ns; e += kWideThreads)
+      for (int e = tid; e < ns; e += (NW * kW))
         if (open(e)) s.pos[e] = 0;
       out = Stop{base_m, base_p, false};
       return true;
@@ -272,7 +272,7 @@ __device__ bool wide_hist(const Lds& s, WideShared& x, int ns, const StopTest& t
     const int mk = __builtin_amdgcn_readlane(mb, bk);
     const double pk = rl_d(pb, bk);
     const double nlo = rl_d(vmin, bk), nhi = rl_d(vmax, bk);
-    for (int e = tid; e < ns; e += kWideThreads)
+    for (int e = tid; e < ns; e += (NW * kW))
       if (open(e)) {
         const int b = bin(s.sl[e].x);
         s.pos[e] = b > bk ? 1 : (b < bk ? 0 : 2);
@@ -287,14 +287,14 @@ __device__ bool wide_hist(const Lds& s, WideShared& x, int ns, const StopTest& t
     // the bin's nodes in generation order: per-chunk counts, then a scatter
     const int nchk = (ns + kW - 1) / kW;
     __syncthreads();                         // classification done; chunk counts free
-    for (int k = w; k < nchk; k += kWideWaves) {
+    for (int k = w; k < nchk; k += NW) {
       const int e = k * kW + lane;
       const unsigned long long gm = __ballot(e < ns && s.pos[e < ns ? e : 0] == 2);
       if (lane == 0) x.ctot[k] = __popcll(gm);
     }
     __syncthreads();
     const ChunkPrefix pre = chunk_prefix(x, nchk, lane);
-    for (int k = w; k < nchk; k += kWideWaves) {
+    for (int k = w; k < nchk; k += NW) {
       const int e = k * kW + lane;
       const bool g = e < ns && s.pos[e < ns ? e : 0] == 2;
       const unsigned long long gm = __ballot(g);
@@ -316,7 +316,8 @@ __device__ bool wide_hist(const Lds& s, WideShared& x, int ns, const StopTest& t
   return false;
 }
 
-__global__ void __launch_bounds__(kWideThreads)
+template <int NW>
+__global__ void __launch_bounds__(NW * kW)
 expand_wide_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict__ topk_logit,
                    const double* __restrict__ lse, int L, int K, int cap, CostTables ct, int fixed, int setcap,
                    int32_t* __restrict__ token_ids, int32_t* __restrict__ parent_out,
@@ -333,7 +334,7 @@ expand_wide_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict
   const RoundCost rc = round_cost(ct, b);
 
   // setup: the top-K table to LDS; A_d = sum_{i<=d} LSE_i in depth order, by wavefront 0
-  for (int i = tid; i < LK; i += kWideThreads) {
+  for (int i = tid; i < LK; i += (NW * kW)) {
     s.tl[i] = topk_logit[(int64_t)b * LK + i];
     s.tid[i] = topk_ids[(int64_t)b * LK + i];
   }
@@ -392,7 +393,7 @@ expand_wide_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict
       const int nchk = (lb - la + kW - 1) / kW;
       // a. each parent's children that reach tau (a prefix of its ranks), and the chunk totals
       int mycut = 0;
-      for (int k = w; k < nchk; k += kWideWaves) {
+      for (int k = w; k < nchk; k += NW) {
         const int p = la + k * kW + lane;
         const bool live = p < lb;
         const double2 pv = s.sl[live ? p : la];
@@ -415,14 +416,14 @@ expand_wide_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict
       const int nb = lb;
       if (nb + pre.tot > setcap) {           // the level would overflow the set: raise tau in place
         if (++raises > kMaxRaises) { failed = true; break; }
-        const double t2 = wide_raise(s, x, la, lb, K, d, Ad, tau, top, keep_hi, need, lane, w, tid);
+        const double t2 = wide_raise<NW>(s, x, la, lb, K, d, Ad, tau, top, keep_hi, need, lane, w, tid);
         if (!(t2 > tau)) { failed = true; break; }
         tau = t2;
         dropped = true;
         continue;                            // build depth d + 1 again
       }
       // b. the children, at their chunk's offset plus the prefix within the chunk
-      for (int k = w; k < nchk; k += kWideWaves) {
+      for (int k = w; k < nchk; k += NW) {
         const int p = la + k * kW + lane;
         const bool live = p < lb;
         const double2 pv = s.sl[live ? p : la];
@@ -457,7 +458,7 @@ expand_wide_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict
     Stop st;
     const unsigned seed = 0x9E3779B9u ^ (unsigned)b ^ ((unsigned)attempt << 16);
     bool have = false;
-    if (ns > 2 * kW) have = wide_hist(s, x, ns, tst, tau, top, lane, w, tid, st);
+    if (ns > 2 * kW) have = wide_hist<NW>(s, x, ns, tst, tau, top, lane, w, tid, st);
     if (!have) {                             // small sets, and the bisection fallback: wavefront 0
       __syncthreads();
       if (w == 0) {
@@ -519,7 +520,7 @@ expand_wide_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict
   // ---- breadth-first positions: kept nodes before each one in generation order
   const int nchk = (ns + kW - 1) / kW;
   __syncthreads();                          // the selection's flags are written
-  for (int k = w; k < nchk; k += kWideWaves) {
+  for (int k = w; k < nchk; k += NW) {
     const int i = k * kW + lane;
     const bool kept = i < ns && (all_kept || s.pos[i < ns ? i : 0] != 0);
     const unsigned long long km = __ballot(kept);
@@ -527,7 +528,7 @@ expand_wide_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict
   }
   __syncthreads();
   const ChunkPrefix pre = chunk_prefix(x, nchk, lane);
-  for (int k = w; k < nchk; k += kWideWaves) {
+  for (int k = w; k < nchk; k += NW) {
     const int i = k * kW + lane;
     const bool live = i < ns;
     const bool kept = live && (all_kept || s.pos[live ? i : 0] != 0);
@@ -536,7 +537,7 @@ expand_wide_kernel(const int32_t* __restrict__ topk_ids, const float* __restrict
   }
   __syncthreads();
   const int64_t ob = (int64_t)b * cap;
-  for (int i = tid; i < ns; i += kWideThreads) {
+  for (int i = tid; i < ns; i += (NW * kW)) {
     const int o = s.pos[i];
     if (o >= 0) {
       const uint32_t m = s.meta[i];
@@ -558,16 +559,29 @@ size_t expand_wide_lds_bytes(int32_t L, int32_t K, int32_t set_cap) {
 }
 
 hipError_t expand_wide_prepare() {
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(&expand_wide_kernel),
-                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)kWideMaxLds);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&expand_wide_kernel<8>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)kWideMaxLds);
+  if (e == hipSuccess)
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&expand_wide_kernel<16>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kWideMaxLds);
+  return e;
 }
 
+// Sixteen wavefronts per round (at most 128 VGPRs each, so one round per CU) when every round has
+// a CU of its own or the set's LDS allows only one round per CU anyway; else eight, so that two
+// rounds share a CU.
 hipError_t launch_expand_wide(const ExpandArgs& a, hipStream_t stream) {
   if (a.B == 0) return hipSuccess;
-  hipLaunchKernelGGL(expand_wide_kernel, dim3((unsigned)a.B), dim3(kWideThreads),
-                     expand_wide_lds_bytes(a.L, a.K, a.level_set_cap), stream, a.topk_ids, a.topk_logit, a.lse, a.L,
-                     a.K, a.cap, a.cost, a.fixed_budget ? 1 : 0, a.level_set_cap, a.token_ids, a.parent, a.depth,
-                     a.path_prob, a.n_star, a.phi, a.theta);
+  const size_t lds = expand_wide_lds_bytes(a.L, a.K, a.level_set_cap);
+  const bool sixteen = a.B <= (int64_t)a.num_cu || 2 * lds > (size_t)160 * 1024;
+  if (sixteen)
+    hipLaunchKernelGGL(expand_wide_kernel<16>, dim3((unsigned)a.B), dim3(16 * kW), lds, stream, a.topk_ids,
+                       a.topk_logit, a.lse, a.L, a.K, a.cap, a.cost, a.fixed_budget ? 1 : 0, a.level_set_cap,
+                       a.token_ids, a.parent, a.depth, a.path_prob, a.n_star, a.phi, a.theta);
+  else
+    hipLaunchKernelGGL(expand_wide_kernel<8>, dim3((unsigned)a.B), dim3(8 * kW), lds, stream, a.topk_ids,
+                       a.topk_logit, a.lse, a.L, a.K, a.cap, a.cost, a.fixed_budget ? 1 : 0, a.level_set_cap,
+                       a.token_ids, a.parent, a.depth, a.path_prob, a.n_star, a.phi, a.theta);
   return hipGetLastError();
 }
 

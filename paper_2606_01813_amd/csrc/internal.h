@@ -51,6 +51,7 @@ struct ExpandArgs {
   float* theta;            // optional
   bool use_level;          // try the batched kernel first
   bool use_wide;           // ... in its several-wavefront form (large trees of a known size)
+  int32_t num_cu;          // compute units of the device
   int32_t level_set_cap;   // its threshold-set capacity
   bool fixed_budget;       // no stop rule: keep the top min(cap, #nodes) nodes (DDTree)
   bool flat_cost;          // every table holds one value: C(n) = C(0) up to the cap

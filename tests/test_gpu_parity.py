@@ -723,10 +723,12 @@ def test_fixed_budget_paths_agree(monkeypatch):
     ("c1", dict(V=2000, B=6, cap=4096, fixed=True)),          # the largest budget, 5120-node set
     ("s1", dict(V=2000, B=6)),                                # cost flat to the cap 4096
     ("s1", dict(V=2000, B=8, L=12, cap=700)),                 # flat cost, shorter trees
+    ("c1", dict(V=1000, B=300, cap=600, fixed=True)),         # more rounds than CUs: eight wavefronts
 ])
 def test_wide_and_one_wave_kernels_agree(name, kw, monkeypatch):
-    """Large trees of a known size run on eight wavefronts per round; the one-wavefront kernel
-    (CADDTREE_EXPAND=level) and the serial kernel give the same trees."""
+    """Large trees of a known size run on 8 or 16 wavefronts per round (16 while every round has a
+    CU of its own); the one-wavefront kernel (CADDTREE_EXPAND=level) and the serial kernel give
+    the same trees."""
     cfg = synth.get_config(name).replace(**kw)
     xs = synth.draw_batch(cfg)
     lg = torch_logits(cfg, xs)
@@ -737,7 +739,8 @@ def test_wide_and_one_wave_kernels_agree(name, kw, monkeypatch):
         else:
             monkeypatch.setenv("CADDTREE_EXPAND", mode)
         outs[mode] = host(run_build(make_plan(cfg), lg))
-    say(f"[wide] {cfg.name} cap {cfg.cap} n* {outs['auto']['n_star'].tolist()}")
+    n = outs["auto"]["n_star"]
+    say(f"[wide] {cfg.name} cap {cfg.cap} B {cfg.B} n* min {n.min()} max {n.max()}")
     _paths_agree({"auto": outs["auto"], "serial": outs["level"]})
     _paths_agree({"auto": outs["auto"], "serial": outs["serial"]})
 
