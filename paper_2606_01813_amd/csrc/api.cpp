@@ -199,6 +199,7 @@ caddtree_status_t run_emit(const caddtree_plan* p, const int32_t* parent, const 
   a.mask_kind = p->mask;
   a.mask = p->mask == CADDTREE_MASK_NONE ? nullptr : mask;
   a.pos_ids = pos_ids;
+  a.num_cu = p->num_cu;
   if (a.mask == nullptr && a.pos_ids == nullptr) return CADDTREE_OK;
   hipError_t e = caddtree::launch_emit(a, stream);
   if (e != hipSuccess) return hip_fail(e, "emit launch");

@@ -93,6 +93,7 @@ struct EmitArgs {
   caddtree_mask_t mask_kind;
   void* mask;              // optional
   int32_t* pos_ids;        // optional
+  int32_t num_cu;          // compute units of the device
 };
 hipError_t launch_emit(const EmitArgs& a, hipStream_t stream);
 
