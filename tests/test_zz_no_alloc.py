@@ -66,6 +66,15 @@ def test_noalloc_on_another_plan():
     _same(ref, got, "c4 shape")
 
 
+def test_noalloc_on_a_wide_kernel_plan():
+    cfg = synth.get_config("s1").replace(V=2000, B=6)      # cost flat to cap 4096: 16 wavefronts per round
+    plan = make_plan(cfg)
+    say("[noalloc] s1-shaped plan, 6 rounds of V = 2000")
+    ref, got = _both(plan, torch_logits(cfg, synth.draw_batch(cfg)))
+    _same(ref, got, "s1 shape")
+    assert ref["n_star"].min() == cfg.cap
+
+
 def test_noalloc_limit():
     import torch
     cfg = synth.get_config("c1").replace(V=16, cap=8)
