@@ -365,6 +365,8 @@ int expand_level_set_cap(int32_t need, bool lean) {
 
 int expand_level_max_need(bool lean) { return lean ? kMaxLeanSet * 4 / 5 : kMaxSet / 2; }
 
+size_t expand_level_lds_limit() { return kMaxLds; }
+
 hipError_t expand_level_prepare() {
   return hipFuncSetAttribute(reinterpret_cast<const void*>(&expand_level_kernel),
                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);

@@ -69,17 +69,20 @@ hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream);
 hipError_t launch_expand_level(const ExpandArgs& a, size_t in_place_lds, hipStream_t stream);
 // the largest serial layout that the batched kernel reserves LDS for
 constexpr size_t kInPlaceLds = 64 * 1024;
+// ... or any serial layout the batched kernels' LDS limit admits, when every round has a CU of its
+// own (reserving it then costs no occupancy)
+size_t expand_level_lds_limit();
 // (lean: fixed budgets and flat costs, which need no cost table and so hold larger sets)
 size_t expand_level_lds_bytes(int32_t L, int32_t K, int32_t set_cap, bool lean);
 int expand_level_set_cap(int32_t need, bool lean);   // threshold-set capacity for trees of at least `need` nodes
 int expand_level_max_need(bool lean);                // the largest `need` the batched kernel takes
 hipError_t expand_level_prepare();        // raises the batched kernel's dynamic-LDS limit
 // The several-wavefront batched kernel (expand_wide.hip): trees that keep a known number of nodes
-// (a fixed budget, or a cost flat up to the cap) of at least 512.  Rounds it cannot settle are
-// flagged n_star = -1 for the serial kernel.
+// (a fixed budget, or a cost flat up to the cap) of at least 512.
 bool expand_wide_applies(int32_t cap, bool lean);
 size_t expand_wide_lds_bytes(int32_t L, int32_t K, int32_t set_cap);
 hipError_t expand_wide_prepare();
+// Rounds it cannot settle are flagged (n_star = -1) for the serial kernel.
 hipError_t launch_expand_wide(const ExpandArgs& a, hipStream_t stream);
 
 // Stage 3: mask and position ids.
