@@ -532,6 +532,26 @@ def test_random_shapes(i):
     _parity_batch(cfg, list(range(cfg.B)), pos_offset=pos_offset, pad=pad)
 
 
+def random_wide_case(i):
+    """A seeded random workload for the several-wavefront expansion: a fixed budget or a cost flat to
+    the cap, of 512 to 1600 nodes, with any L, K, V, dtype and mask."""
+    rng = np.random.default_rng(9100 + i)
+    K = int(rng.integers(2, 17))
+    fixed = bool(rng.random() < 0.5)
+    cfg = synth.get_config("c1").replace(
+        name=f"wide{i}", B=int(rng.integers(1, 5)), L=int(rng.integers(4, 33)), K=K,
+        V=int(rng.integers(max(K, 64), 3001)), cap=int(rng.integers(512, 1601)),
+        dtype=("f32", "bf16")[int(rng.integers(0, 2))], mask=("u8", "bits")[int(rng.integers(0, 2))],
+        cost="c4" if fixed else "const", fixed=fixed, seed=synth.configs.SEED_BASE + 9100 + i)
+    return cfg, int(rng.integers(0, 100)), int(rng.choice([0, 0, 1, 3]))
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_random_wide_shapes(i):
+    cfg, pos_offset, pad = random_wide_case(i)
+    _parity_batch(cfg, list(range(cfg.B)), pos_offset=pos_offset, pad=pad)
+
+
 # ------------------------------------------------------------- full-size workloads
 
 def _full_size(name, sample=None, workers=16):
