@@ -18,8 +18,9 @@
 // (>= K) disjoint lane groups of the group maximum over the first chunks, which
 // is <= the K-th largest element, so no top-K element is ever filtered out.
 //
-// At the end, wave 0 merges the waves' lists (each candidate ranked against all of
-// them in one pass when they fit in one wave), combines the per-wave sums,
+// At the end, wave 0 merges the waves' lists (when their K best fit in one wave, each
+// candidate, as a 64-bit key, is ranked against all of them in one pass), combines the
+// per-wave sums,
 // and replaces the top-K terms' fp32 exp2 values (recomputed bit-identically
 // from the exponent recorded at insertion) by fp64 values, which removes the
 // error of the largest terms from the normaliser.
@@ -207,8 +208,21 @@ __device__ __forceinline__ unsigned load_guarded(const T* rowp, int e, int V, fl
   return ok;
 }
 
-// kUnroll: 16-byte loads in flight per lane (4 or 8)
-template <typename T, bool kAligned, int kUnroll>
+// (value, id) as one unsigned 64-bit key whose order is the top-K order: the value's bits mapped
+// to an unsigned integer that grows with the value, then INT_MAX - id (smaller ids first)
+__device__ __forceinline__ uint64_t order_key(float v, int id) {
+  const uint32_t b = (uint32_t)__float_as_int(v);
+  const uint32_t u = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+  return ((uint64_t)u << 32) | (uint32_t)(INT_MAX - id);
+}
+__device__ __forceinline__ float key_value(uint64_t k) {
+  const uint32_t u = (uint32_t)(k >> 32);
+  return __int_as_float((int)((u & 0x80000000u) ? (u & 0x7fffffffu) : ~u));
+}
+__device__ __forceinline__ int key_id(uint64_t k) { return INT_MAX - (int)(uint32_t)k; }
+
+// kUnroll: 16-byte loads in flight per lane (4 or 8); kS: wavefronts per row (1 .. 16)
+template <typename T, bool kAligned, int kUnroll, int kS>
 __global__ void __launch_bounds__(1024)
 reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int K,
                    int32_t* __restrict__ out_ids, float* __restrict__ out_logit,
@@ -220,10 +234,13 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
   __shared__ float s_lv[16][16];
   __shared__ int s_lid[16][16];
   __shared__ float s_lr[16][16];
+  __shared__ uint64_t s_key[kWave];     // the waves' K best as keys, wave w's at w K .. w K + K - 1
+  __shared__ float s_kr[kWave];
+  __shared__ int s_sel[16];
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
-  const int S = blockDim.x / kWave;
+  constexpr int S = kS;
   const int64_t row = blockIdx.x;
   const T* rowp = logits + row * row_stride;
   const int nch = (V + CH - 1) / CH;
@@ -303,7 +320,13 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
 
   // wave sum of the per-lane accumulators (fixed order: a DPP scan, the total in the last lane)
   const double acc = xp::rl_d(xp::wave_incl_scan(s.acc), kWave - 1);
-  if (lane < 16) { s_lv[wave][lane] = s.lv; s_lid[wave][lane] = s.lid; s_lr[wave][lane] = s.lr; }
+  if (S > 1) {
+    if (S * K <= kWave) {
+      if (lane < K) { s_key[wave * K + lane] = order_key(s.lv, s.lid); s_kr[wave * K + lane] = s.lr; }
+    } else if (lane < 16) {
+      s_lv[wave][lane] = s.lv; s_lid[wave][lane] = s.lid; s_lr[wave][lane] = s.lr;
+    }
+  }
   if (lane == 0) { s_acc[wave] = acc; s_r[wave] = s.r; }
   __syncthreads();
   if (wave != 0) return;
@@ -311,17 +334,28 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
   if (S == 1) {
     // one wave per row: its list is the row's
   } else if (S * K <= kWave) {
-    // every wave's K best, one per lane: a lane's rank among them (ids are distinct) is its slot in
-    // the merged list; only slots below K are needed, and those hold real entries
-    const bool has = lane < S * K;
-    const int w = has ? lane / K : 0, k = has ? lane % K : 0;
-    const float v = has ? s_lv[w][k] : -INFINITY;
-    const int id = has ? s_lid[w][k] : INT_MAX;
-    const float rr = has ? s_lr[w][k] : 0.f;
+    // every wave's K best, one per lane: a lane's rank among them (keys are distinct, as ids are) is
+    // its slot in the merged list; only slots below K are needed, and those hold real entries
+    const int n = S * K;
+    const bool has = lane < n;
+    const uint64_t key = has ? s_key[lane] : 0ull;
+    const uint32_t klo = (uint32_t)key, khi = (uint32_t)(key >> 32);
     int rank = 0;
-    for (int j = 0; j < S * K; ++j) rank += before(readlane_f(v, j), readlane_i(id, j), v, id) ? 1 : 0;
-    if (has && rank < K) { s_lv[0][rank] = v; s_lid[0][rank] = id; s_lr[0][rank] = rr; }
-    if (lane < K) { s.lv = s_lv[0][lane]; s.lid = s_lid[0][lane]; s.lr = s_lr[0][lane]; }
+#pragma unroll
+    for (int j = 0; j < S * 16 && j < kWave; ++j) {
+      if (j < n) {
+        const uint64_t kj = ((uint64_t)(uint32_t)readlane_i((int)khi, j) << 32) | (uint32_t)readlane_i((int)klo, j);
+        rank += kj > key ? 1 : 0;
+      }
+    }
+    if (has && rank < K) s_sel[rank] = lane;
+    if (lane < K) {
+      const int src = s_sel[lane];
+      const uint64_t kk = s_key[src];
+      s.lv = key_value(kk);
+      s.lid = key_id(kk);
+      s.lr = s_kr[src];
+    }
   } else {
     for (int w = 1; w < S; ++w) {
       for (int k = 0; k < K; ++k) {
@@ -334,8 +368,10 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
     }
   }
   float R = s_r[0];
+#pragma unroll
   for (int w = 1; w < S; ++w) R = fmaxf(R, s_r[w]);
   double sum = 0.0;
+#pragma unroll
   for (int w = 0; w < S; ++w) sum += ldexp(s_acc[w], (int)fmaxf(s_r[w] - R, -2000.f));
   double corr = 0.0;
   if (lane < K) {
@@ -354,19 +390,28 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
   if (lane == 0) out_lse[row] = lse;
 }
 
+template <typename T, bool A, int U, int S>
+void launch_s(const ReduceArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL((reduce_topk_kernel<T, A, U, S>), dim3((unsigned)a.rows), dim3((unsigned)(kWave * S)), 0, stream,
+                     static_cast<const T*>(a.logits), a.row_stride, a.V, a.K, a.ids, a.logit, a.lq, a.lse);
+}
+
+template <typename T, bool A, int U>
+hipError_t launch_u(const ReduceArgs& a, hipStream_t stream) {
+  switch (a.waves_per_row) {
+    case 1: launch_s<T, A, U, 1>(a, stream); break;
+    case 2: launch_s<T, A, U, 2>(a, stream); break;
+    case 4: launch_s<T, A, U, 4>(a, stream); break;
+    case 8: launch_s<T, A, U, 8>(a, stream); break;
+    case 16: launch_s<T, A, U, 16>(a, stream); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 template <typename T, bool A>
 hipError_t launch_t(const ReduceArgs& a, hipStream_t stream) {
-  const dim3 grid((unsigned)a.rows);
-  const dim3 block((unsigned)(kWave * a.waves_per_row));
-  if (a.unroll == 8)
-    hipLaunchKernelGGL((reduce_topk_kernel<T, A, 8>), grid, block, 0, stream,
-                       static_cast<const T*>(a.logits), a.row_stride, a.V, a.K,
-                       a.ids, a.logit, a.lq, a.lse);
-  else
-    hipLaunchKernelGGL((reduce_topk_kernel<T, A, 4>), grid, block, 0, stream,
-                       static_cast<const T*>(a.logits), a.row_stride, a.V, a.K,
-                       a.ids, a.logit, a.lq, a.lse);
-  return hipGetLastError();
+  return a.unroll == 8 ? launch_u<T, A, 8>(a, stream) : launch_u<T, A, 4>(a, stream);
 }
 
 }  // namespace
