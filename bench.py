@@ -452,6 +452,10 @@ def main():
         "stages_us": {"reduce_topk": float(k1s.mean()), "expand": float(k2.mean()), "emit": float(k3.mean())},
         "stages_median_us": {"reduce_topk": float(np.median(k1s)), "expand": float(np.median(k2)),
                              "emit": float(np.median(k3))},
+        # the expansion is a dependent chain per round, with no bandwidth or flop roofline: its batch time,
+        # that time per round, and the nodes the batch keeps per second of it
+        "expand": {"median_us_per_batch": float(np.median(k2)), "us_per_round": float(np.median(k2)) / B,
+                   "nodes_kept": int(ns.sum()), "nodes_kept_per_s": float(ns.sum()) / (float(np.median(k2)) * 1e-6)},
         "step_us": {"gpu_mean": gpu_step_us,
                     "with_per_step_events": {"median": med_step, "min": float(step_us.min()),
                                              "max": float(step_us.max()), "rounds_per_s_at_median": B / (med_step * 1e-6),

@@ -348,6 +348,9 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
         rank += kj > key ? 1 : 0;
       }
     }
+    // the row holds at least K elements, so slots 0 .. K - 1 each receive exactly one lane; the first
+    // store only keeps every slot a valid index
+    if (lane < K) s_sel[lane] = lane;
     if (has && rank < K) s_sel[rank] = lane;
     if (lane < K) {
       const int src = s_sel[lane];
