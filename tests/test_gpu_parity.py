@@ -928,6 +928,16 @@ def test_plan_from_fitted_profiles():
     compare_tree(h, rs, cfg.mask, cfg.cap)
 
 
+@pytest.mark.parametrize("waves", [2, 4, 8, 16])
+def test_k1_merge_with_short_segments(waves, monkeypatch):
+    """Rows split over more wavefronts than they have chunks: some segments are empty or hold fewer than K
+    elements, so their lists end part empty and the merge ranks padding entries among the real ones."""
+    monkeypatch.setenv("CADDTREE_K1_WAVES", str(waves))
+    for kw in (dict(V=40, K=16, L=4, cap=64, B=4), dict(V=16, K=16, L=4, cap=600, B=3, cost="tiny"),
+               dict(V=1100, K=8, L=5, cap=64, B=4)):
+        _parity_batch(synth.get_config("c1").replace(**kw), list(range(kw["B"])))
+
+
 @pytest.mark.parametrize("waves", [1, 2, 4, 8, 16])
 @pytest.mark.parametrize("unroll", [4, 8])
 def test_k1_launch_shapes(waves, unroll, monkeypatch):
