@@ -334,8 +334,9 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
   if (S == 1) {
     // one wave per row: its list is the row's
   } else if (S * K <= kWave) {
-    // every wave's K best, one per lane: a lane's rank among them (keys are distinct, as ids are) is
-    // its slot in the merged list; only slots below K are needed, and those hold real entries
+    // every wave's K best, one per lane: a lane's rank among them is its slot in the merged list.  Real
+    // entries have distinct keys (ids are distinct); the padding of a segment with fewer than K elements
+    // shares one key below every real one.  Only slots below K are needed, and those hold real entries
     const int n = S * K;
     const bool has = lane < n;
     const uint64_t key = has ? s_key[lane] : 0ull;
