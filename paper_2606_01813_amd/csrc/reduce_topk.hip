@@ -209,15 +209,13 @@ __device__ __forceinline__ unsigned load_guarded(const T* rowp, int e, int V, fl
 }
 
 // (value, id) as one unsigned 64-bit key whose order is the top-K order: the value's bits mapped
-// to an unsigned integer that grows with the value, then INT_MAX - id (smaller ids first)
+// to an unsigned integer that grows with the value (-0 taken as +0, which compares equal to it),
+// then INT_MAX - id (smaller ids first)
 __device__ __forceinline__ uint64_t order_key(float v, int id) {
-  const uint32_t b = (uint32_t)__float_as_int(v);
+  uint32_t b = (uint32_t)__float_as_int(v);
+  if (b == 0x80000000u) b = 0u;
   const uint32_t u = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
   return ((uint64_t)u << 32) | (uint32_t)(INT_MAX - id);
-}
-__device__ __forceinline__ float key_value(uint64_t k) {
-  const uint32_t u = (uint32_t)(k >> 32);
-  return __int_as_float((int)((u & 0x80000000u) ? (u & 0x7fffffffu) : ~u));
 }
 __device__ __forceinline__ int key_id(uint64_t k) { return INT_MAX - (int)(uint32_t)k; }
 
@@ -235,6 +233,7 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
   __shared__ int s_lid[16][16];
   __shared__ float s_lr[16][16];
   __shared__ uint64_t s_key[kWave];     // the waves' K best as keys, wave w's at w K .. w K + K - 1
+  __shared__ float s_kv[kWave];         // ... their values as read (the sign of a zero included)
   __shared__ float s_kr[kWave];
   __shared__ int s_sel[16];
 
@@ -322,7 +321,11 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
   const double acc = xp::rl_d(xp::wave_incl_scan(s.acc), kWave - 1);
   if (S > 1) {
     if (S * K <= kWave) {
-      if (lane < K) { s_key[wave * K + lane] = order_key(s.lv, s.lid); s_kr[wave * K + lane] = s.lr; }
+      if (lane < K) {
+        s_key[wave * K + lane] = order_key(s.lv, s.lid);
+        s_kv[wave * K + lane] = s.lv;
+        s_kr[wave * K + lane] = s.lr;
+      }
     } else if (lane < 16) {
       s_lv[wave][lane] = s.lv; s_lid[wave][lane] = s.lid; s_lr[wave][lane] = s.lr;
     }
@@ -355,9 +358,8 @@ reduce_topk_kernel(const T* __restrict__ logits, int64_t row_stride, int V, int 
     if (has && rank < K) s_sel[rank] = lane;
     if (lane < K) {
       const int src = s_sel[lane];
-      const uint64_t kk = s_key[src];
-      s.lv = key_value(kk);
-      s.lid = key_id(kk);
+      s.lid = key_id(s_key[src]);
+      s.lv = s_kv[src];
       s.lr = s_kr[src];
     }
   } else {

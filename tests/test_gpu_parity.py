@@ -316,6 +316,37 @@ def test_bf16_ties():
     compare_tree(host(out2), rs, cfg.mask, cfg.cap)
 
 
+@pytest.mark.parametrize("waves", [1, 4, 16])
+def test_k1_signed_zero_ties(waves, monkeypatch):
+    """Rows whose K-th largest logit is a zero shared by +0 and -0 entries: the two compare equal, so the
+    ids decide, in every wavefront's list and in the merge of the lists."""
+    import oracle
+    import torch
+    monkeypatch.setenv("CADDTREE_K1_WAVES", str(waves))
+    for dtype in ("f32", "bf16"):
+        cfg = synth.get_config("c1").replace(V=9000, B=3, L=4, K=8, dtype=dtype)
+        rng = np.random.default_rng(11)
+        x32 = (-1.0 - rng.random((cfg.B, cfg.L, cfg.V))).astype(np.float32)   # all below -1
+        for b in range(cfg.B):
+            for i in range(cfg.L):
+                top = rng.choice(cfg.V, 3, replace=False)
+                x32[b, i, top] = 1.0 + rng.random(3).astype(np.float32)           # three above 0
+                zeros = rng.choice(np.setdiff1d(np.arange(cfg.V), top), 12, replace=False)
+                x32[b, i, zeros[:6]] = 0.0
+                x32[b, i, zeros[6:]] = -0.0                                      # twelve zeros of both signs
+        xs = synth.bf16_bits_from_f32(x32) if dtype == "bf16" else x32
+        plan = make_plan(cfg)
+        out = plan.new_outputs(cfg.B, topk=True)
+        plan.reduce_topk(torch_logits(cfg, xs), out.topk_ids, out.topk_logit, out.lse, out.topk_lq)
+        torch.cuda.synchronize()
+        h = host(out)
+        for b in range(cfg.B):
+            m = oracle.marginals(xs[b], dtype, cfg.K)
+            assert np.array_equal(h["topk_ids"][b], m["ids"]), (dtype, b)
+            assert np.array_equal(h["topk_logit"][b].astype(np.float64), m["logit"]), (dtype, b)
+            assert np.abs(h["lse"][b] - m["lse"]).max() <= 1e-7
+
+
 def test_determinism():
     cfg = synth.get_config("c1").replace(V=40000, B=12)
     xs = synth.draw_batch(cfg)
