@@ -2,8 +2,8 @@
 
 Small cases (several tiles, ragged tails, every dtype / mask / special case) and
 the full-size workloads (run in the launch configuration the benchmark times)
-are compared element by element on every round; only the 4096-node trees of the
-constant-cost stress case and a 70,000-round grid test are compared on samples.
+are compared element by element on every round; only a 70,000-round grid test is
+compared on a sample.
 Properties that hold at any size are checked on every round.  Rounds are drawn
 through the input guard (tests/_guard.py), so every floating-point decision of a
 compared round keeps a margin of at least 1e-6, more for deep trees.
@@ -646,9 +646,8 @@ def test_full_s2():
 
 
 def test_full_s1():
-    # a constant cost keeps every node up to the cap: 4096-node trees in the lean layout
-    rng = np.random.default_rng(7)
-    _full_size("s1", sorted({0, 131, 255} | set(rng.choice(256, 29, replace=False).tolist())))
+    # a constant cost keeps every node up to the cap: 4096-node trees in the lean layout, every round
+    _full_size("s1")
 
 
 # ------------------------------------------------------------- context-aware cost (Sec. 4.6)
