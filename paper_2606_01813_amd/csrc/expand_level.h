@@ -185,28 +185,73 @@ __device__ void cut_group_flags(const Lds& s, int ns, const double (&sg)[P], dou
   }
 }
 
-// up to 64 nodes: rank by sigma (ties by index), Phi by a prefix sum over those positions;
-// on a stop inside the set, the kept flags go to s.pos by generation index
+// ---- sigma values in pop order by a bitonic network across the wave: the delta at a pop position, and
+// with it Phi and the stop test there, depend only on the sigma values in descending order (nodes that
+// tie on sigma have equal deltas), so the network sorts the values alone.
+
+// the value of lane `lane ^ J`: DPP within a row of 16 lanes (XOR 4 and 8 as two permutations each),
+// an LDS permute across rows
+template <int J>
+__device__ __forceinline__ int xor_lane_i(int v) {
+  if constexpr (J == 1) return dpp_i<0xB1, 0xF, false>(0, v);                       // quad_perm [1,0,3,2]
+  else if constexpr (J == 2) return dpp_i<0x4E, 0xF, false>(0, v);                  // quad_perm [2,3,0,1]
+  else if constexpr (J == 4) return dpp_i<0x141, 0xF, false>(0, dpp_i<0x1B, 0xF, false>(0, v));  // half mirror o [3,2,1,0]
+  else if constexpr (J == 8) return dpp_i<0x141, 0xF, false>(0, dpp_i<0x140, 0xF, false>(0, v)); // half mirror o mirror
+  else return __shfl_xor(v, J);
+}
+template <int J>
+__device__ __forceinline__ double xor_lane(double v) {
+  const uint64_t u = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = (uint32_t)xor_lane_i<J>((int)(uint32_t)u);
+  const uint32_t hi = (uint32_t)xor_lane_i<J>((int)(uint32_t)(u >> 32));
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// one compare-exchange stage (block size KB, distance J) over element e = r * 64 + lane of v[r]
+template <int P, int KB, int J>
+__device__ __forceinline__ void sort_stage(double (&v)[P], int lane) {
+  if constexpr (J >= kW) {
+    constexpr int jr = J / kW;
+#pragma unroll
+    for (int r = 0; r < P; ++r) {
+      if ((r ^ jr) > r) {
+        const bool desc = ((r * kW + lane) & KB) == 0;
+        const double a = v[r], b = v[r ^ jr];
+        const double hi = fmax(a, b), lo = fmin(a, b);
+        v[r] = desc ? hi : lo;
+        v[r ^ jr] = desc ? lo : hi;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < P; ++r) {
+      const double o = xor_lane<J>(v[r]);
+      const bool keep_max = ((lane & J) == 0) == (((r * kW + lane) & KB) == 0);
+      v[r] = keep_max ? fmax(v[r], o) : fmin(v[r], o);
+    }
+  }
+}
+template <int P, int KB, int J>
+__device__ __forceinline__ void sort_merge(double (&v)[P], int lane) {
+  sort_stage<P, KB, J>(v, lane);
+  if constexpr (J > 1) sort_merge<P, KB, J / 2>(v, lane);
+}
+template <int P, int KB = 2>
+__device__ __forceinline__ void sort_desc(double (&v)[P], int lane) {
+  sort_merge<P, KB, KB / 2>(v, lane);
+  if constexpr (KB < P * kW) sort_desc<P, KB * 2>(v, lane);
+}
+
+// up to 64 nodes: the sigma values in pop order, Phi by a prefix sum over those positions; on a stop
+// inside the set, the kept flags go to s.pos by generation index
 __device__ Stop stop_small(const Lds& s, int ns, const StopTest& tst, int lane) {
   const bool live = lane < ns;
   double sg[1];
   sg[0] = live ? s.sl[lane].x : -INFINITY;
   const double me = sg[0];
-  int r = 0;
-  int o = 0;
-  for (; o + 4 <= ns; o += 4) {
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const double so = rl_d(me, o + u);
-      r += (int)(so > me) | ((int)(so == me) & (int)(o + u < lane));
-    }
-  }
-  for (; o < ns; ++o) {
-    const double so = rl_d(me, o);
-    r += (int)(so > me) | ((int)(so == me) & (int)(o < lane));
-  }
-  if (live) s.dl[r] = exp(me);
-  const double d = live ? s.dl[lane] : 0.0;   // delta at position `lane`
+  double srt[1] = {me};
+  sort_desc<1>(srt, lane);                    // lane p: sigma at pop position p (padding last)
+  const double d = live ? exp(srt[0]) : 0.0;  // delta at position `lane`
   const double incl = wave_incl_scan(d);
   const double pe = wave_shr1(incl);          // Phi before position `lane`
   const bool keep = live && kept_at(lane, pe, d, tst);
@@ -214,7 +259,7 @@ __device__ Stop stop_small(const Lds& s, int ns, const StopTest& tst, int lane) 
   if (!fm) return Stop{ns, rl_d(incl, kW - 1), true};
   const int stop = __builtin_ctzll(fm);
   // the tie group at the stop position
-  const double v = rl_d(me, __builtin_ctzll(__ballot(live && r == stop)));
+  const double v = rl_d(srt[0], stop);
   const int g0 = __popcll(__ballot(live && me > v));
   if (g0 < stop) {
     cut_group_flags<1>(s, ns, sg, v, g0, stop, lane);
@@ -236,74 +281,48 @@ __device__ __forceinline__ int group_stop(int mA, double phA, double dA, int tA,
   return tA;
 }
 
-// Sets of 65 .. 64 P nodes held in registers (node e = j * 64 + lane): every node's position in
-// sigma order (ties by index) by one counting pass over the set, each value read from its lane;
-// the path probabilities are scattered into that order, and the stop test runs at every
-// position in parallel, 64 positions at a time, with Phi carried across them.
+// Sets of 65 .. 64 P nodes held in registers (node e = j * 64 + lane): the sigma values in pop order by
+// the network over 64 P positions (position p = j * 64 + lane in register j), and the stop test at
+// every position in parallel, 64 positions at a time, with Phi carried across them.
 template <int P>
 __device__ Stop stop_rank(const Lds& s, int ns, const StopTest& tst, int lane) {
-  double sg[P];
-  int r[P];
+  double sg[P], srt[P];
 #pragma unroll
   for (int j = 0; j < P; ++j) {
     const int e = j * kW + lane;
     sg[j] = e < ns ? s.sl[e].x : -INFINITY;
-    r[j] = 0;
+    srt[j] = sg[j];
   }
-  // node o = jo * 64 + ol is read from its lane (jo is a compile-time index once unrolled); it
-  // precedes node e = j * 64 + lane if its sigma is larger, or equal with o < e, which holds for
-  // every o of an earlier block and for no o of a later one
-#pragma unroll
-  for (int jo = 0; jo < P; ++jo) {
-    const int lim = ns - jo * kW < kW ? ns - jo * kW : kW;   // wave-uniform
-    auto count = [&](double so, int ol) {
-#pragma unroll
-      for (int j = 0; j < P; ++j) {
-        if (jo < j) r[j] += (int)(so >= sg[j]);
-        else if (jo > j) r[j] += (int)(so > sg[j]);
-        else r[j] += (int)(so > sg[j]) | ((int)(so == sg[j]) & (int)(ol < lane));
-      }
-    };
-    int ol = 0;
-    for (; ol + 4 <= lim; ol += 4) {
-      double so[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) so[u] = rl_d(sg[jo], ol + u);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) count(so[u], ol + u);
-    }
-    for (; ol < lim; ++ol) count(rl_d(sg[jo], ol), ol);
-  }
-#pragma unroll
-  for (int j = 0; j < P; ++j)
-    if (j * kW + lane < ns) s.dl[r[j]] = exp(sg[j]);
+  sort_desc<P>(srt, lane);
   double carry = 0.0;                         // Phi before the current 64 positions
   int stop = ns;
   double phi = 0.0;
-  for (int p0 = 0; p0 < ns; p0 += kW) {
-    const int p = p0 + lane;
-    const bool live = p < ns;
-    const double d = live ? s.dl[p] : 0.0;
-    const double incl = wave_incl_scan(d);
-    const double pe = carry + wave_shr1(incl);  // Phi before position p
-    const bool keep = live && kept_at(p, pe, d, tst);
-    const unsigned long long fm = __ballot(live && !keep);
-    if (fm) {
-      const int l = __builtin_ctzll(fm);
-      stop = p0 + l;
-      phi = rl_d(pe, l);
-      break;
+#pragma unroll
+  for (int j = 0; j < P; ++j) {
+    const int p0 = j * kW;
+    if (p0 < ns && stop == ns) {              // wave-uniform
+      const int p = p0 + lane;
+      const bool live = p < ns;
+      const double d = live ? exp(srt[j]) : 0.0;
+      const double incl = wave_incl_scan(d);
+      const double pe = carry + wave_shr1(incl);  // Phi before position p
+      const bool keep = live && kept_at(p, pe, d, tst);
+      const unsigned long long fm = __ballot(live && !keep);
+      if (fm) {
+        const int l = __builtin_ctzll(fm);
+        stop = p0 + l;
+        phi = rl_d(pe, l);
+      } else {
+        carry += rl_d(incl, kW - 1);
+      }
     }
-    carry += rl_d(incl, kW - 1);
   }
   if (stop == ns) return Stop{ns, carry, true};
   // the tie group at the stop position
   double v = 0.0;
 #pragma unroll
-  for (int j = 0; j < P; ++j) {
-    const unsigned long long m = __ballot(j * kW + lane < ns && r[j] == stop);
-    if (m) v = rl_d(sg[j], __builtin_ctzll(m));
-  }
+  for (int j = 0; j < P; ++j)
+    if (stop / kW == j) v = rl_d(srt[j], stop % kW);
   int g0 = 0;
 #pragma unroll
   for (int j = 0; j < P; ++j) g0 += __popcll(__ballot(sg[j] > v));
