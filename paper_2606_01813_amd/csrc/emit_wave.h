@@ -6,11 +6,14 @@
 // packed masks: words below ceil(n / 32), the bits at or beyond n as zero), as
 // the stand-alone emission kernel does.
 //
-// Rows go in tiles of 64: lane r walks row r's ancestor chain (strictly
-// decreasing indices in breadth-first order, at most CADDTREE_MAX_L steps) and
-// sets one bit per ancestor in its own row of an LDS bit tile; the tile is then
-// stored with consecutive lanes on consecutive words (packed) or 16-byte column
-// groups (dense u8, 16 bits spread to 16 bytes).
+// Trees of at most 64 nodes: lane i holds row i as a 64-bit mask and gathers its
+// ancestors by pointer jumping (row |= row of the node 2^k levels up, k = 0, 1, ..:
+// log2 of the depth rounds of lane permutes instead of a dependent LDS read per
+// depth), then writes its own row.  Larger trees go in tiles of 64 rows: lane r
+// walks row r's ancestor chain (strictly decreasing indices in breadth-first order,
+// at most CADDTREE_MAX_L steps) and sets one bit per ancestor in its own row of an
+// LDS bit tile; the tile is then stored with consecutive lanes on consecutive words
+// (packed) or 16-byte column groups (dense u8, 16 bits spread to 16 bytes).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -46,6 +49,45 @@ __device__ __forceinline__ void emit_mask_wave(const int16_t* par, int n, int ca
   if (n <= 0 || mask == nullptr || mask_kind == CADDTREE_MASK_NONE) return;
   const int tw = (n + 31) >> 5;                  // words per tile row = words written per mask row
   const int stride = (cap + 31) >> 5;            // words per packed mask row
+  if (n <= 64) {
+    const bool live = lane < n;
+    int p = live ? (int)par[lane] : -1;
+    if (p >= lane) p = -1;                       // a malformed parent array ends the chain
+    uint64_t row = live ? (1ull << lane) : 0ull;
+    // after round k, row holds the node and its 2^(k+1) - 1 nearest ancestors, and p the next one up
+    for (int k = 0; k < 8 && __ballot(p >= 0); ++k) {
+      const int src = p >= 0 ? p : lane;
+      const uint32_t alo = (uint32_t)__shfl((int)(uint32_t)row, src);
+      const uint32_t ahi = (uint32_t)__shfl((int)(uint32_t)(row >> 32), src);
+      const int ap = __shfl(p, src);
+      if (p >= 0) {
+        row |= ((uint64_t)ahi << 32) | alo;
+        p = ap;
+      }
+    }
+    if (!live) return;
+    if (mask_kind == CADDTREE_MASK_BITS32) {
+      uint32_t* m = static_cast<uint32_t*>(mask) + (int64_t)lane * stride;
+      for (int w = 0; w < tw; ++w) m[w] = (uint32_t)(row >> (32 * w));
+    } else {
+      uint8_t* rowp = static_cast<uint8_t*>(mask) + (int64_t)lane * cap;
+      for (int c0 = 0; c0 < n; c0 += 16) {
+        const uint32_t bits = (uint32_t)(row >> c0) & 0xFFFFu;
+        const int c1 = c0 + 16 < n ? c0 + 16 : n;
+        if (c1 - c0 == 16 && (reinterpret_cast<uintptr_t>(rowp + c0) & 15u) == 0) {
+          uint4 q;
+          q.x = emit_spread4(bits);
+          q.y = emit_spread4(bits >> 4);
+          q.z = emit_spread4(bits >> 8);
+          q.w = emit_spread4(bits >> 12);
+          *reinterpret_cast<uint4*>(rowp + c0) = q;
+        } else {
+          for (int c = c0; c < c1; ++c) rowp[c] = (uint8_t)((bits >> (c - c0)) & 1u);
+        }
+      }
+    }
+    return;
+  }
   for (int r0 = 0; r0 < n; r0 += 64) {
     const int nr = n - r0 < 64 ? n - r0 : 64;
     for (int w = lane; w < nr * tw; w += 64) tile[w] = 0u;
