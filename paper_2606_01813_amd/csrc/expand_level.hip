@@ -7,10 +7,14 @@
 // workgroup (one wavefront) per round:
 //
 //  1. build T(tau) level by level from the root.  The children of a node that
-//     reach the threshold are a prefix of its ranks (sigma falls with the rank),
-//     so each lane counts its node's children, stopping at the first rank that
-//     no lane takes; a prefix sum gives their slots, and the set comes out in
-//     breadth-first order (depth, then rank tuple), which is also the
+//     reach the threshold are a prefix of its ranks (sigma falls with the rank).
+//     A level of few parents (at most 256 (parent, rank) pairs) is tested one
+//     pair a lane, kW / K parents a pass and four passes at once; lane order is
+//     (parent, rank) order, so a qualifying child's slot is the count of
+//     qualifying lanes below it.  A wider level takes one parent a lane, each
+//     lane counting its node's children up to the first rank that no lane
+//     takes, and a prefix sum gives their slots.  Either way the set comes out
+//     in breadth-first order (depth, then rank tuple), which is also the
 //     tie-break of the pop order within a depth.  When a level would not fit
 //     in the set, tau is raised in place: a histogram of sigma over the levels
 //     built and the candidates of the next one picks the new threshold, the
@@ -23,11 +27,10 @@
 //     depends only on the sigma values in descending order.  The rest of the
 //     order decides only which members are kept of a tie group that the stop
 //     cuts:
-//     * up to 64 nodes: each lane ranks its node by sigma (ties by index), the
-//       path probabilities are scattered into that order, a prefix sum gives
-//       Phi before every position m, and m is kept iff
+//     * up to 128 nodes: a bitonic network across the wave sorts the sigma
+//       values (one or two a lane), a prefix sum of their path probabilities
+//       gives Phi before every position m, and m is kept iff
 //       (1 + Phi_m + delta_m) / C(m + 1) > (1 + Phi_m) / C(m) and m < cap;
-//     * 65 to 128 nodes: the same, with every node ranked by one counting pass;
 //     * larger sets: under a convex cost theta rises and then falls along the
 //       pop order (Thm. 1), so the stop test fails from n* on.  A 64-bin
 //       histogram of sigma gives the position of each bin's first node and
@@ -88,6 +91,13 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   const bool lean = fixed || flat;          // no cost table
   const Lds s = carve(smem, (size_t)LK, (size_t)setcap, lean);
   const RoundCost rc = round_cost(ct, b);
+  // the level build's lane split: group grp of K lanes takes one parent, lane rk of it one rank
+  constexpr int kPasses = 4;               // passes a step
+  constexpr int kPairsFew = 256;           // levels of at most this many (parent, rank) pairs go by pairs
+  const int ppass = kW / K;                 // parents a pass (K <= 16: at least 4)
+  const int grp = lane / K;
+  const int rk = lane - grp * K;
+  const bool in_pass = grp < ppass;
 
   // setup: the round's global loads are issued together, then stored to LDS.  Indices are
   // clamped rather than guarded (a clamped lane loads and stores the same value as the last
@@ -210,39 +220,80 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
     for (int d = 1; d < L && la < lb;) {
       const double Ad = rl_d(Areg, d + 1);
       const int tli = d * K + (lane < K ? lane : K - 1);
+      const double tr = (double)s.tl[d * K + rk];     // rank rk at depth d + 1
       int nb = lb;
       bool over = false;
-      for (int p0 = la; p0 < lb; p0 += kW) {
-        const int p = p0 + lane;
-        const bool live = p < lb;
-        const double2 pv = s.sl[live ? p : la];
-        // lane r: rank r at depth d + 1, read after the parents (every lane reads a valid entry, so
-        // no branch holds the read back and the two reads overlap)
-        const double tlv = lane < K ? (double)s.tl[tli] : 0.0;
-        // the ranks that qualify form a prefix: count them rank by rank until no lane takes one
-        // (dead lanes compute too, on a valid node, and are masked out of the count)
-        int c = 0, rmax = 0;
-        for (; rmax < K; ++rmax) {
-          const double x = (pv.y + rl_d(tlv, rmax)) - Ad;
-          const int q = (int)(x >= tau) & (int)live;
-          if (__ballot(q != 0) == 0) break;
-          c += q;
-        }
-        const int incl = wave_incl_scan(c);
-        const int tot = __builtin_amdgcn_readlane(incl, kW - 1);
-        const int off = incl - c;
-        if (live && c < K) cut = true;
-        if (nb + tot > setcap) { over = true; break; }
-        for (int r = 0; r < rmax; ++r) {
-          const double l = pv.y + rl_d(tlv, r);
-          const double2 v = make_double2(pmin(l - Ad, pv.x), l);
-          const uint32_t m = pack(p, r, d + 1);
-          if (r < c) {
-            s.sl[nb + off + r] = v;
-            s.meta[nb + off + r] = m;
+      if ((lb - la) * K <= kPairsFew) {
+        // ppass parents a pass, one lane per (parent, rank): a child's place in the level is the count
+        // of qualifying lanes below it, since lane order is (parent, rank) order.  Four passes go
+        // together, their parents read at once.  Lanes past the level's end (and past ppass K)
+        // compute on a valid node and take no child.
+        for (int q0 = la; q0 < lb; q0 += kPasses * ppass) {
+          double2 pv[kPasses];
+          int p[kPasses];
+          bool live[kPasses];
+#pragma unroll
+          for (int u = 0; u < kPasses; ++u) {
+            p[u] = q0 + u * ppass + grp;
+            live[u] = in_pass && p[u] < lb;
+            pv[u] = s.sl[live[u] ? p[u] : la];
+          }
+          bool q[kPasses];
+          double x[kPasses], l[kPasses];
+          unsigned long long m[kPasses];
+          int tot = 0;
+#pragma unroll
+          for (int u = 0; u < kPasses; ++u) {
+            l[u] = pv[u].y + tr;
+            x[u] = l[u] - Ad;
+            q[u] = live[u] && x[u] >= tau;
+            if (live[u] && !q[u]) cut = true;  // a child of a node of the set is left out
+            m[u] = __ballot(q[u]);
+            tot += __popcll(m[u]);
+          }
+          if (nb + tot > setcap) { over = true; break; }
+#pragma unroll
+          for (int u = 0; u < kPasses; ++u) {
+            if (q[u]) {
+              const int at = nb + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m[u] >> 32),
+                                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)m[u], 0u));
+              s.sl[at] = make_double2(pmin(x[u], pv[u].x), l[u]);
+              s.meta[at] = pack(p[u], rk, d + 1);
+            }
+            nb += __popcll(m[u]);
           }
         }
-        nb += tot;
+      } else {
+        // one lane per parent: the ranks that qualify form a prefix, counted rank by rank until no
+        // lane takes one (dead lanes compute too, on a valid node, and are masked out of the count)
+        for (int p0 = la; p0 < lb; p0 += kW) {
+          const int p = p0 + lane;
+          const bool live = p < lb;
+          const double2 pv = s.sl[live ? p : la];
+          const double tlv = lane < K ? (double)s.tl[tli] : 0.0;   // lane r: rank r at depth d + 1
+          int c = 0, rmax = 0;
+          for (; rmax < K; ++rmax) {
+            const double x = (pv.y + rl_d(tlv, rmax)) - Ad;
+            const int q = (int)(x >= tau) & (int)live;
+            if (__ballot(q != 0) == 0) break;
+            c += q;
+          }
+          const int incl = wave_incl_scan(c);
+          const int tot = __builtin_amdgcn_readlane(incl, kW - 1);
+          const int off = incl - c;
+          if (live && c < K) cut = true;
+          if (nb + tot > setcap) { over = true; break; }
+          for (int r = 0; r < rmax; ++r) {
+            const double l = pv.y + rl_d(tlv, r);
+            const double2 v = make_double2(pmin(l - Ad, pv.x), l);
+            const uint32_t m = pack(p, r, d + 1);
+            if (r < c) {
+              s.sl[nb + off + r] = v;
+              s.meta[nb + off + r] = m;
+            }
+          }
+          nb += tot;
+        }
       }
       if (over) {
         const double tlv = lane < K ? (double)s.tl[tli] : 0.0;
