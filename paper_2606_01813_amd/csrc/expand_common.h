@@ -78,11 +78,13 @@ struct RoundCost {
   double alpha;
   double t_draft;
 
-  __device__ __forceinline__ double operator()(int n) const {
+  // C(n) from the two tables' entries lo[n] and hi[n]
+  __device__ __forceinline__ double mix(double l, double h) const {
 #pragma clang fp contract(off)
-    const double cv = (1.0 - alpha) * lo[n] + alpha * hi[n];
+    const double cv = (1.0 - alpha) * l + alpha * h;
     return t_draft + cv;
   }
+  __device__ __forceinline__ double operator()(int n) const { return mix(lo[n], hi[n]); }
 };
 
 // The cost of round b (CostTables, the plan's tables as the kernels see them, is in kargs.h).

@@ -110,15 +110,20 @@ struct CostCache {
     constexpr int kC = 8;                    // entries per lane and batch
     const int hi = ((k + kW - 1) / kW) * kW < ncw ? ((k + kW - 1) / kW) * kW : ncw;
     for (int i0 = filled; i0 < hi; i0 += kC * kW) {
-      double cv[kC];
+      double lv[kC], hv[kC];
       int ci[kC];
 #pragma unroll
       for (int u = 0; u < kC; ++u) {        // clamped, not guarded, so the loads go out together;
         ci[u] = i0 + u * kW + lane < hi ? i0 + u * kW + lane : hi - 1;   // past the end, every
-        cv[u] = rc(ci[u] < cap ? ci[u] : cap);                             // lane reads one entry
+        const int n = ci[u] < cap ? ci[u] : cap;                           // lane reads one entry
+        lv[u] = rc.lo[n];
+        hv[u] = rc.hi[n];
       }
+      // every load is issued before the first use: a use waits for all loads issued before it
+      // (and for the caller's, e.g. the top-K table's), so an interleaved use would cost a round trip
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int u = 0; u < kC; ++u) cw[ci[u]] = cv[u];
+      for (int u = 0; u < kC; ++u) cw[ci[u]] = rc.mix(lv[u], hv[u]);
     }
     filled = hi;
   }
