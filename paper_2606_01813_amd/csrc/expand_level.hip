@@ -94,6 +94,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   // the level build's lane split: group grp of K lanes takes one parent, lane rk of it one rank
   constexpr int kPasses = 4;               // passes a step
   constexpr int kPairsFew = 256;           // levels of at most this many (parent, rank) pairs go by pairs
+  constexpr int kSoftMul = 2;              // soft set limit of a round of known size, in keep_hi
   const int ppass = kW / K;                 // parents a pass (K <= 16: at least 4)
   const int grp = lane / K;
   const int rk = lane - grp * K;
@@ -204,6 +205,12 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       keep_hi = need <= 1 || half > mid ? half : mid;
     }
     if (keep_hi > setcap) keep_hi = setcap;
+    // a flat start (a round that keeps a known number of nodes before any stop test) raises tau
+    // as soon as the set passes soft, well above keep_hi, rather than when it would overflow:
+    // building and selecting in a set many times the tree costs more than the raise.  A raise from
+    // there that finds no threshold drops the limit.
+    int soft = setcap;
+    if (tight && !lean && kSoftMul * keep_hi + kW < setcap) soft = kSoftMul * keep_hi + kW;
     // ---- 1. T(tau), level by level
     bool cut = false;
     {
@@ -251,7 +258,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
             m[u] = __ballot(q[u]);
             tot += __popcll(m[u]);
           }
-          if (nb + tot > setcap) { over = true; break; }
+          if (nb + tot > soft) { over = true; break; }
 #pragma unroll
           for (int u = 0; u < kPasses; ++u) {
             if (q[u]) {
@@ -282,7 +289,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
           const int tot = __builtin_amdgcn_readlane(incl, kW - 1);
           const int off = incl - c;
           if (live && c < K) cut = true;
-          if (nb + tot > setcap) { over = true; break; }
+          if (nb + tot > soft) { over = true; break; }
           for (int r = 0; r < rmax; ++r) {
             const double l = pv.y + rl_d(tlv, r);
             const double2 v = make_double2(pmin(l - Ad, pv.x), l);
@@ -298,7 +305,15 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
       if (over) {
         const double tlv = lane < K ? (double)s.tl[tli] : 0.0;
         const double t2 = ++raises > kMaxRaises ? NAN : raise_tau(s, la, lb, K, Ad, tlv, tau, top, keep_hi, need, lane);
-        if (!(t2 > tau)) { failed = true; break; }
+        if (!(t2 > tau)) {
+          if (soft < setcap) {                 // nothing changed: build the level again up to setcap
+            soft = setcap;
+            raises = 0;
+            continue;
+          }
+          failed = true;
+          break;
+        }
         tau = t2;
         cut = true;                          // nodes were dropped: the tree continues below tau
         continue;                            // build depth d + 1 again
