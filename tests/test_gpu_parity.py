@@ -395,13 +395,20 @@ def test_plan_before_torch_in_a_fresh_process():
     dict(cost="const", cap=100, fixed=False),   # grows to the cap through a tie group of 256
     dict(cost="c4", cap=100, fixed=True),       # fixed budget through the same ties
     dict(cost="const", cap=340, fixed=False),   # the whole tree (4 + 16 + 64 + 256 nodes)
+    # a flat start to 64 whose first set (16 + 256 nodes) passes the early-raise limit, where no
+    # threshold keeps between 65 and 89 nodes: the raise fails, the limit is dropped, and the stop
+    # cuts the tie group of depth 2 at 64
+    dict(cost="c3", cap=300, fixed=False, K=16, V=20),
 ])
 def test_constant_logits(kw):
     """Every logit equal: all nodes of a depth tie on sigma and Lambda, so the pop order inside a
-    depth is the rank tuple alone, and the cap cuts a group of equal nodes.  No decision depends on
-    the normaliser's rounding (depths differ by ln V in sigma; a flat cost or a fixed budget never
-    stops before the cap), so the oracle's tree is compared without the input guard."""
-    cfg = synth.get_config("c0").replace(B=3, L=4, V=1000, K=4, dtype="f32", mask="bits", **kw)
+    depth is the rank tuple alone, and the cap (or the stop) cuts a group of equal nodes.  No
+    decision depends on the normaliser's rounding (depths differ by ln V in sigma; a flat cost or a
+    fixed budget never stops before the cap, and the flat start's stop after 64 nodes has a margin
+    of about one half), so the oracle's tree is compared without the input guard."""
+    shape = dict(B=3, L=4, V=1000, K=4, dtype="f32", mask="bits")
+    shape.update(kw)
+    cfg = synth.get_config("c0").replace(**shape)
     x = np.zeros((cfg.B, cfg.L, cfg.V), dtype=np.float32)
     x[1] += 2.5                                   # a constant shift changes nothing
     x[2] -= 7.0
