@@ -65,6 +65,11 @@ def _piecewise_c3(n: np.ndarray) -> np.ndarray:
                              1.768 + 0.012 * (n - 256)))
 
 
+def _flat_then_rise(f: int) -> Callable[[np.ndarray], np.ndarray]:
+    # flat at 1.0 up to n = f, then a convex rise (the marginal grows from 0.004)
+    return lambda n: np.where(n <= f, 1.0, 1.0 + 0.004 * (n - f) + 0.00002 * (n - f) * (n - f))
+
+
 _COSTS: Dict[str, Callable[[np.ndarray], np.ndarray]] = {
     "c0": _quad(0.01, 0.0005),
     "c1": _quad(0.002, 0.00002),
@@ -72,6 +77,11 @@ _COSTS: Dict[str, Callable[[np.ndarray], np.ndarray]] = {
     "c4": _quad(0.001, 0.000005),
     "const": lambda n: np.ones_like(n, dtype=np.float64),
     "tiny": lambda n: 1.0 + 1e-6 * n,          # almost flat: trees of hundreds of nodes
+    # flat starts of other lengths than c3's 64 (test workloads)
+    "flat16": _flat_then_rise(16),
+    "flat32": _flat_then_rise(32),
+    "flat128": _flat_then_rise(128),
+    "flat200": _flat_then_rise(200),
 }
 
 

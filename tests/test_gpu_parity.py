@@ -570,6 +570,29 @@ def test_random_shapes(i):
     _parity_batch(cfg, list(range(cfg.B)), pos_offset=pos_offset, pad=pad)
 
 
+def random_flat_case(i):
+    """A seeded random workload with a flat cost start of 16 to 200 nodes (every tree keeps that many
+    before any stop test), so the batched expansion's early raise and its restarts run under many
+    shapes: any L, K, V, dtype and mask, sharp (deep) or temperature-mixed rows."""
+    rng = np.random.default_rng(9300 + i)
+    base = synth.get_config(("c3", "s2")[i % 2])
+    K = int(rng.integers(2, 17))
+    cost = str(rng.choice(["flat16", "flat32", "flat128", "flat200"]))
+    flat = int(cost[4:])
+    cfg = base.replace(
+        name=f"flat{i}", B=int(rng.integers(2, 7)), L=int(rng.integers(3, 33)), K=K,
+        V=int(rng.integers(max(K, 64), 6001)), cap=int(rng.integers(flat + 1, 701)),
+        dtype=("f32", "bf16")[int(rng.integers(0, 2))], mask=("u8", "bits")[int(rng.integers(0, 2))],
+        cost=cost, fixed=False, seed=synth.configs.SEED_BASE + 9300 + i)
+    return cfg, int(rng.integers(0, 100))
+
+
+@pytest.mark.parametrize("i", range(16))
+def test_random_flat_starts(i):
+    cfg, pos_offset = random_flat_case(i)
+    _parity_batch(cfg, list(range(cfg.B)), pos_offset=pos_offset)
+
+
 def random_wide_case(i):
     """A seeded random workload for the several-wavefront expansion: a fixed budget or a cost flat to
     the cap, of 512 to 1600 nodes, with any L, K, V, dtype and mask."""

@@ -60,6 +60,10 @@ def test_cost_tables():
     assert np.all(np.diff(d) >= -1e-12)     # convex up to rounding
     c1 = synth.cost_table(synth.get_config("c1"))
     assert len(c1) == 513 and c1[10] == 1.0 + 0.002 * 10 + 0.00002 * 100
+    for f in (16, 32, 128, 200):
+        t = synth.cost_table(f"flat{f}", 700)
+        assert np.all(t[:f + 1] == 1.0) and t[f + 1] > 1.0      # flat up to f, rising after
+        assert np.all(np.diff(np.diff(t)) >= -1e-12)            # convex up to rounding
 
 
 @pytest.mark.parametrize("name", ["c0", "c1", "c2", "c3", "c4"])
