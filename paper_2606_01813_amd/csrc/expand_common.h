@@ -105,5 +105,33 @@ __device__ __forceinline__ RoundCost round_cost(const CostTables& ct, int64_t b)
   return c;
 }
 
+// round_cost computed by a whole wavefront (all 64 lanes call it; J <= 64): the context length and
+// every grid point are loaded at once, lane j taking L_j, and the grid points at or below l are
+// counted with one ballot, so the search takes one round trip instead of one per grid step.  The
+// same table choice and alpha as round_cost.
+__device__ __forceinline__ RoundCost round_cost_wave(const CostTables& ct, int64_t b, int lane) {
+  RoundCost c{ct.tv, ct.tv, 0.0, ct.t_draft};
+  if (ct.J >= 2) {
+    const int64_t ell = ct.ctx_len[b];
+    const int64_t g = ct.grid[lane < ct.J ? lane : ct.J - 1];
+    const int below = __popcll(__ballot(lane < ct.J && g <= ell));   // L_0 .. L_{below - 1} <= l
+    auto lane_i64 = [&](int l) -> int64_t {
+      const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)g, l);
+      const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)g >> 32), l);
+      return (int64_t)(((uint64_t)hi << 32) | lo);
+    };
+    if (below >= ct.J) {                                             // l >= L_{J-1}
+      c.lo = c.hi = ct.tv + (int64_t)(ct.J - 1) * ct.stride;
+    } else if (below >= 1 && ell > lane_i64(0)) {                    // L_0 < l < L_{J-1}
+      const int j = below - 1;                                       // L_j <= l < L_{j+1}
+      const int64_t gj = lane_i64(j), gj1 = lane_i64(j + 1);
+      c.lo = ct.tv + (int64_t)j * ct.stride;
+      c.hi = c.lo + ct.stride;
+      c.alpha = (double)(ell - gj) / (double)(gj1 - gj);
+    }
+  }
+  return c;
+}
+
 }  // namespace xp
 }  // namespace caddtree

@@ -90,7 +90,7 @@ expand_level_kernel(const int32_t* __restrict__ topk_ids, const float* __restric
   const int LK = L * K;
   const bool lean = fixed || flat;          // no cost table
   const Lds s = carve(smem, (size_t)LK, (size_t)setcap, lean);
-  const RoundCost rc = round_cost(ct, b);
+  const RoundCost rc = round_cost_wave(ct, b, lane);
   // the level build's lane split: group grp of K lanes takes one parent, lane rk of it one rank
   constexpr int kPasses = 4;               // passes a step
   constexpr int kPairsFew = 256;           // levels of at most this many (parent, rank) pairs go by pairs
